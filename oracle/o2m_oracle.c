@@ -1,0 +1,369 @@
+/*
+ * CPU oracle for 2M + Ozaki-II complex GEMM.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or calls
+ * this file; only the test suite, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code, header, table or constant with the HIP
+ * library: every number here is derived from the paper's definitions on its
+ * own.
+ *
+ * Three plain, slow, obviously correct computations:
+ *
+ *  oracle_gauss_4m  C = AB over Gaussian integers by the classical 4M
+ *                   expansion (Section 1), exact in 128-bit integers.  This is
+ *                   the result 2M reaches exactly in integer mode (Section 2:
+ *                   once the modulus bounds |Re c|, |Im c|, C mod m determines C).
+ *
+ *  oracle_oq_gemm   The exact output of Algorithm 1 ("2M Ozaki-II"),
+ *                   written as its plain definition.  The integer products are
+ *                   exact and the CRT + symmetric lift recover the integer
+ *                   product C = A_int B_int exactly whenever every |Re c|,
+ *                   |Im c| <= (M-1)/2 (Section 3.1), which the scaling budget
+ *                   guarantees.  So Algorithm 1 returns
+ *                     round_fp64(A_int B_int) * 2^(E_i + F_j - pA - pB)
+ *                   with A_int = round_Z(a * 2^(pA - E_i)) (step 3, componentwise,
+ *                   ties to even), computed here in exact multiword integers
+ *                   by 4M.  The moduli only enter through pA, pB, which the
+ *                   caller derives from M (Python side).
+ *
+ *  oracle_dd_gemm   The product of the unquantized inputs by 4M in
+ *                   double-double (error ~ k 2^-104 |A||B|): the reference the
+ *                   accuracy of the method is measured against (Section 6).
+ *
+ * Matrices are column-major, complex interleaved (re, im), with leading
+ * dimensions in complex elements.  Exponent rule (the paper leaves the choice
+ * of sigma, tau open, Section 3.1/3.2): E_i is the frexp exponent of the
+ * largest |Re| or |Im| in row i of A (so that max < 2^E_i), 0 for a zero row;
+ * F_j likewise for column j of B.  A row or column holding Inf or NaN makes
+ * its whole row or column of C NaN.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef __int128 i128;
+typedef unsigned __int128 u128;
+
+/* ------------------------------------------------------------------------ */
+/* exact integer helpers                                                     */
+/* ------------------------------------------------------------------------ */
+
+/* 256-bit two's complement accumulator, little-endian 64-bit words. */
+typedef struct { uint64_t w[4]; } acc256;
+
+static void acc_add_shifted(acc256 *a, i128 v, int shift) {
+    /* a += v * 2^shift, 0 <= shift < 128 */
+    uint64_t x[4];
+    int neg = v < 0;
+    u128 uv = (u128)v;
+    x[0] = (uint64_t)uv;
+    x[1] = (uint64_t)(uv >> 64);
+    x[2] = x[3] = neg ? ~0ULL : 0ULL;
+    while (shift >= 64) {
+        x[3] = x[2]; x[2] = x[1]; x[1] = x[0]; x[0] = 0;
+        shift -= 64;
+    }
+    if (shift > 0) {
+        x[3] = (x[3] << shift) | (x[2] >> (64 - shift));
+        x[2] = (x[2] << shift) | (x[1] >> (64 - shift));
+        x[1] = (x[1] << shift) | (x[0] >> (64 - shift));
+        x[0] = x[0] << shift;
+    }
+    unsigned carry = 0;
+    for (int t = 0; t < 4; ++t) {
+        u128 s = (u128)a->w[t] + x[t] + carry;
+        a->w[t] = (uint64_t)s;
+        carry = (unsigned)(s >> 64);
+    }
+}
+
+/* Round a 256-bit signed integer to the nearest double, ties to even. */
+static double acc_to_double(const acc256 *a) {
+    uint64_t w[4];
+    memcpy(w, a->w, sizeof w);
+    int neg = (int64_t)w[3] < 0;
+    if (neg) { /* two's complement negate */
+        unsigned carry = 1;
+        for (int t = 0; t < 4; ++t) {
+            u128 s = (u128)(~w[t]) + carry;
+            w[t] = (uint64_t)s;
+            carry = (unsigned)(s >> 64);
+        }
+    }
+    int top = -1;
+    for (int t = 3; t >= 0; --t)
+        if (w[t]) { top = 64 * t + 63 - __builtin_clzll(w[t]); break; }
+    if (top < 0) return 0.0;
+    double r;
+    if (top <= 52) {
+        r = (double)w[0];                      /* exact */
+    } else {
+        int sh = top - 52;                     /* bits below the 53-bit mantissa */
+        /* mantissa = bits [sh, sh+52] */
+        uint64_t mant = 0;
+        for (int b = 0; b < 53; ++b) {
+            int bit = sh + b;
+            if ((w[bit >> 6] >> (bit & 63)) & 1ULL) mant |= 1ULL << b;
+        }
+        int rbit = sh - 1;
+        int round_bit = (int)((w[rbit >> 6] >> (rbit & 63)) & 1ULL);
+        int sticky = 0;
+        for (int bit = 0; bit < rbit && !sticky; ++bit)
+            if ((w[bit >> 6] >> (bit & 63)) & 1ULL) sticky = 1;
+        if (round_bit && (sticky || (mant & 1ULL))) mant += 1; /* may reach 2^53: still exact */
+        r = ldexp((double)mant, sh);
+    }
+    return neg ? -r : r;
+}
+
+static void acc_from_i128(acc256 *a, i128 v) {
+    memset(a, 0, sizeof *a);
+    acc_add_shifted(a, v, 0);
+}
+
+/* ------------------------------------------------------------------------ */
+/* scaling exponents                                                         */
+/* ------------------------------------------------------------------------ */
+
+/* value x = mant * 2^shift exactly, |mant| <= 2^53, shift >= 0 */
+typedef struct { int64_t mant; int shift; } qint;
+
+static qint to_qint(double x) {
+    qint q;
+    if (fabs(x) < 9007199254740992.0) { /* 2^53: plain integer */
+        q.mant = (int64_t)x;
+        q.shift = 0;
+    } else {
+        int e;
+        double f = frexp(x, &e);                 /* x = f * 2^e, |f| in [0.5,1) */
+        q.mant = (int64_t)ldexp(f, 53);          /* exact: x is an integer with e >= 54 */
+        q.shift = e - 53;
+    }
+    return q;
+}
+
+/* Exponent of one complex vector: max over |re|,|im|; returns flag for non-finite. */
+static int vec_exponent(const double *x, long stride, int len, int *nonfinite) {
+    double amax = 0.0;
+    int bad = 0;
+    for (int t = 0; t < len; ++t) {
+        double re = x[2 * (long)t * stride], im = x[2 * (long)t * stride + 1];
+        if (!isfinite(re) || !isfinite(im)) bad = 1;
+        double a = fmax(fabs(re), fabs(im));
+        if (a > amax) amax = a;
+    }
+    *nonfinite = bad;
+    if (bad || amax == 0.0) return 0;
+    int e;
+    frexp(amax, &e);
+    return e;
+}
+
+/* Quantize one complex entry: round_Z[i] componentwise, RN-even (Algorithm 1, step 3). */
+static void quantize(const double *src, int shift, qint *re, qint *im) {
+    *re = to_qint(rint(ldexp(src[0], shift)));
+    *im = to_qint(rint(ldexp(src[1], shift)));
+}
+
+/* ------------------------------------------------------------------------ */
+/* O-Z: exact Gaussian-integer 4M                                            */
+/* ------------------------------------------------------------------------ */
+
+/* Returns the number of output components that do not fit in int64. */
+int oracle_gauss_4m(int m, int n, int k, const int32_t *A, int lda, const int32_t *B, int ldb,
+                    int64_t *C, int ldc) {
+    int overflow = 0;
+#pragma omp parallel for schedule(dynamic) reduction(+ : overflow)
+    for (int j = 0; j < n; ++j) {
+        for (int i = 0; i < m; ++i) {
+            i128 re = 0, im = 0;
+            for (int p = 0; p < k; ++p) {
+                const int32_t *a = A + 2 * ((long)i + (long)p * lda);
+                const int32_t *b = B + 2 * ((long)p + (long)j * ldb);
+                /* (ar + i ai)(br + i bi) = (ar br - ai bi) + i (ar bi + ai br) */
+                re += (i128)a[0] * b[0] - (i128)a[1] * b[1];
+                im += (i128)a[0] * b[1] + (i128)a[1] * b[0];
+            }
+            if (re > INT64_MAX || re < INT64_MIN) overflow++;
+            if (im > INT64_MAX || im < INT64_MIN) overflow++;
+            C[2 * ((long)i + (long)j * ldc)] = (int64_t)re;
+            C[2 * ((long)i + (long)j * ldc) + 1] = (int64_t)im;
+        }
+    }
+    return overflow;
+}
+
+/* ------------------------------------------------------------------------ */
+/* O-Q: exact output of Algorithm 1                                          */
+/* ------------------------------------------------------------------------ */
+
+/* Exponents of the rows of A (m x k) and columns of B (k x n). */
+void oracle_exponents(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                      int32_t *E, int32_t *Ebad, int32_t *F, int32_t *Fbad) {
+    for (int i = 0; i < m; ++i) {
+        int bad;
+        E[i] = vec_exponent(A + 2 * (long)i, lda, k, &bad);
+        Ebad[i] = bad;
+    }
+    for (int j = 0; j < n; ++j) {
+        int bad;
+        F[j] = vec_exponent(B + 2 * (long)j * ldb, 1, k, &bad);
+        Fbad[j] = bad;
+    }
+}
+
+static void mul_acc(acc256 *acc, i128 *fast, int use_fast, qint x, qint y, int sign) {
+    i128 p = (i128)x.mant * (i128)y.mant;
+    if (sign < 0) p = -p;
+    if (use_fast) *fast += p;
+    else acc_add_shifted(acc, p, x.shift + y.shift);
+}
+
+/*
+ * C (or the listed entries of C) = Algorithm 1 applied to A (m x k), B (k x n)
+ * with quantization shifts pA, pB.  n_entries < 0: the full matrix into C with
+ * leading dimension ldc.  n_entries >= 0: entry t = (ei[t], ej[t]) into
+ * C[2t], C[2t+1].  Also returns, if c_int_out is non-null, the exact integer
+ * products as doubles rounded (same as the unscaled output) -- used by tests.
+ */
+void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                    int pA, int pB, double *C, int ldc, int n_entries, const int32_t *ei,
+                    const int32_t *ej) {
+    int32_t *E = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
+    int32_t *Eb = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
+    int32_t *F = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
+    int32_t *Fb = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
+    oracle_exponents(m, n, k, A, lda, B, ldb, E, Eb, F, Fb);
+
+    /* int128 suffices when no quantized value needs a shift and
+       2k 2^(pA+pB) < 2^126 (bound on every partial sum). */
+    int use_fast = pA <= 53 && pB <= 53 && (pA + pB + 1 + (int)ceil(log2((double)k + 1)) < 126);
+    long total = n_entries < 0 ? (long)m * n : n_entries;
+
+#pragma omp parallel
+    {
+        qint *bre = (qint *)malloc(sizeof(qint) * (k > 0 ? k : 1));
+        qint *bim = (qint *)malloc(sizeof(qint) * (k > 0 ? k : 1));
+        int cached_j = -1;
+#pragma omp for schedule(dynamic, 64)
+        for (long t = 0; t < total; ++t) {
+            int i, j;
+            if (n_entries < 0) { j = (int)(t / m); i = (int)(t % m); }
+            else { i = ei[t]; j = ej[t]; }
+            double *out = n_entries < 0 ? C + 2 * ((long)i + (long)j * ldc) : C + 2 * t;
+            if (Eb[i] || Fb[j]) { out[0] = NAN; out[1] = NAN; continue; }
+            if (j != cached_j) {
+                for (int p = 0; p < k; ++p)
+                    quantize(B + 2 * ((long)p + (long)j * ldb), pB - F[j], &bre[p], &bim[p]);
+                cached_j = j;
+            }
+            acc256 re, im;
+            i128 fre = 0, fim = 0;
+            memset(&re, 0, sizeof re);
+            memset(&im, 0, sizeof im);
+            for (int p = 0; p < k; ++p) {
+                qint are, aim;
+                quantize(A + 2 * ((long)i + (long)p * lda), pA - E[i], &are, &aim);
+                /* 4M: Re = ar br - ai bi, Im = ar bi + ai br */
+                mul_acc(&re, &fre, use_fast, are, bre[p], +1);
+                mul_acc(&re, &fre, use_fast, aim, bim[p], -1);
+                mul_acc(&im, &fim, use_fast, are, bim[p], +1);
+                mul_acc(&im, &fim, use_fast, aim, bre[p], +1);
+            }
+            if (use_fast) { acc_from_i128(&re, fre); acc_from_i128(&im, fim); }
+            int scale = E[i] + F[j] - pA - pB;
+            out[0] = ldexp(acc_to_double(&re), scale);
+            out[1] = ldexp(acc_to_double(&im), scale);
+        }
+        free(bre);
+        free(bim);
+    }
+    free(E); free(Eb); free(F); free(Fb);
+}
+
+/* Exact integer product of the quantized operands, entries only, as 4 signed
+   64-bit words per component (little-endian two's complement): for tests that
+   compare residues. out has 8 words per entry (re then im). */
+void oracle_oq_cint(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                    int pA, int pB, int n_entries, const int32_t *ei, const int32_t *ej,
+                    uint64_t *out) {
+    int32_t *E = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
+    int32_t *Eb = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
+    int32_t *F = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
+    int32_t *Fb = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
+    oracle_exponents(m, n, k, A, lda, B, ldb, E, Eb, F, Fb);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (long t = 0; t < n_entries; ++t) {
+        int i = ei[t], j = ej[t];
+        acc256 re, im;
+        i128 dummy = 0;
+        memset(&re, 0, sizeof re);
+        memset(&im, 0, sizeof im);
+        for (int p = 0; p < k; ++p) {
+            qint are, aim, bre, bim;
+            quantize(A + 2 * ((long)i + (long)p * lda), pA - E[i], &are, &aim);
+            quantize(B + 2 * ((long)p + (long)j * ldb), pB - F[j], &bre, &bim);
+            mul_acc(&re, &dummy, 0, are, bre, +1);
+            mul_acc(&re, &dummy, 0, aim, bim, -1);
+            mul_acc(&im, &dummy, 0, are, bim, +1);
+            mul_acc(&im, &dummy, 0, aim, bre, +1);
+        }
+        memcpy(out + 8 * t, re.w, 32);
+        memcpy(out + 8 * t + 4, im.w, 32);
+    }
+    free(E); free(Eb); free(F); free(Fb);
+}
+
+/* Correct rounding of a signed 128-bit integer given as two words (for pins). */
+double oracle_round_i128(uint64_t lo, uint64_t hi) {
+    acc256 a;
+    i128 v = (i128)(((u128)hi << 64) | lo);
+    acc_from_i128(&a, v);
+    return acc_to_double(&a);
+}
+
+/* ------------------------------------------------------------------------ */
+/* O-F: double-double 4M                                                     */
+/* ------------------------------------------------------------------------ */
+
+static inline void two_sum(double a, double b, double *s, double *e) {
+    double x = a + b, bb = x - a;
+    *e = (a - (x - bb)) + (b - bb);
+    *s = x;
+}
+
+static inline void dd_add_prod(double *hi, double *lo, double a, double b) {
+    double p = a * b;
+    double pe = fma(a, b, -p);
+    double s, e;
+    two_sum(*hi, p, &s, &e);
+    e += *lo + pe;
+    double t = s + e;
+    *lo = e - (t - s);
+    *hi = t;
+}
+
+void oracle_dd_gemm(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                    double *Chi, double *Clo, int ldc, int n_entries, const int32_t *ei,
+                    const int32_t *ej) {
+    long total = n_entries < 0 ? (long)m * n : n_entries;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (long t = 0; t < total; ++t) {
+        int i, j;
+        long o;
+        if (n_entries < 0) { j = (int)(t / m); i = (int)(t % m); o = 2 * ((long)i + (long)j * ldc); }
+        else { i = ei[t]; j = ej[t]; o = 2 * t; }
+        double rh = 0, rl = 0, ih = 0, il = 0;
+        for (int p = 0; p < k; ++p) {
+            const double *a = A + 2 * ((long)i + (long)p * lda);
+            const double *b = B + 2 * ((long)p + (long)j * ldb);
+            dd_add_prod(&rh, &rl, a[0], b[0]);
+            dd_add_prod(&rh, &rl, -a[1], b[1]);
+            dd_add_prod(&ih, &il, a[0], b[1]);
+            dd_add_prod(&ih, &il, a[1], b[0]);
+        }
+        Chi[o] = rh; Clo[o] = rl;
+        Chi[o + 1] = ih; Clo[o + 1] = il;
+    }
+}
