@@ -1,0 +1,156 @@
+/*
+ * o2m.h -- complex GEMM, HERK and SYRK by 2M multiplication combined with the
+ * Ozaki-II scheme, on int8 matrix cores of AMD Instinct MI355X (gfx950).
+ *
+ * Method: "The 2M Multiplication Algorithm for Complex Matrices" (Caday).
+ *   Section 2     2M multiplication: for an odd modulus m with s^2 = -1 (mod m)
+ *                 a complex product of integer matrices modulo m costs two real
+ *                 products, C+ = A+ B+ and C- = A- B- with A+- = Ar +- s Ai.
+ *   Section 3.2   Algorithm 1 ("2M Ozaki-II"): scale rows of A and columns of
+ *                 B by powers of two, quantize to Gaussian integers, run 2M
+ *                 modulo each of N coprime 2M moduli <= 256 (int8 GEMMs), and
+ *                 recover the exact integer product by the Chinese remainder
+ *                 theorem with a symmetric lift, then undo the scaling.
+ *   Section 4     The 2M moduli: the greedy set {241, 233, 229, 221, 205, ...,
+ *                 37, 29} (22 moduli, product ~2^152); N = 16 gives ~2^117.
+ *   Section 5     HERK: C- = C+^T, so one int8 GEMM per modulus; SYRK: A A^T
+ *                 = Re(Z Z^H) with Z = A1 + i A2 (half the k).
+ *
+ * Conventions for every call below
+ *   - Matrices are column-major.  Complex matrices are interleaved (re, im);
+ *     leading dimensions count complex elements.  alpha = 1, beta = 0 (the
+ *     setting of the paper's experiments, Section 6).
+ *   - A, B, C are DEVICE pointers owned by the caller; the library never frees
+ *     or retains them.  C must not overlap A or B.
+ *   - stream is a hipStream_t (NULL = the default stream).  Calls enqueue
+ *     their kernels on it and return without synchronizing; the output is
+ *     ready when the stream reaches that point.
+ *   - n_moduli is N, the number of 2M moduli used (1..22); accuracy grows by
+ *     about 3.7 bits per modulus and int8 GEMM work grows linearly in N.
+ *   - Scaling rule (Algorithm 1 step 2): E_i = frexp exponent of the largest
+ *     |Re| or |Im| in row i of A (F_j: column j of B); P = the largest integer
+ *     with 2k 2^P <= (M-1)/2 - floor(M/2^32); pA = floor(P/2), pB = P - pA
+ *     (HERK/SYRK: pA = pB = floor(P/2)); entries are quantized as
+ *     rint(a 2^(pA - E_i)), ties to even.  The result equals the exact
+ *     integer product of the quantized operands rounded to nearest fp64 and
+ *     scaled by 2^(E_i + F_j - pA - pB) (CGEMM: then rounded to fp32).
+ *   - Rows of A or columns of B containing Inf or NaN give NaN in the
+ *     corresponding rows / columns of C; zero rows or columns give +0.
+ *   - m == 0 or n == 0: nothing is done.  k == 0: C is set to zero.
+ *
+ * Workspace: the library needs device scratch memory for the residue planes
+ * (size: o2m_workspace_bytes).  It allocates it on first use per device and
+ * grows it as needed (hipMalloc, synchronizing the device when it grows); a
+ * caller may instead hand over its own buffer with o2m_set_workspace.
+ * Calls on one device share that workspace: calls that overlap in time on
+ * different streams of the same device race.
+ *
+ * Return value: O2M_OK, or a negative code.  -1 .. -12: the position of the
+ * first invalid argument (BLAS convention, counting from 1).  Errors found
+ * before anything is enqueued leave C untouched.
+ */
+#ifndef O2M_H
+#define O2M_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int o2m_status;
+
+#define O2M_OK 0
+#define O2M_ERR_NMODULI (-20)   /* n_moduli outside 1..22 (gauss mode: 1..8)        */
+#define O2M_ERR_KLIMIT (-21)    /* k > 149130: int32 accumulation could overflow  */
+#define O2M_ERR_WORKSPACE (-22) /* caller workspace too small                       */
+#define O2M_ERR_HIP (-23)       /* a HIP runtime call or kernel launch failed       */
+#define O2M_ERR_NOMEM (-24)     /* workspace allocation failed                      */
+#define O2M_ERR_SIZE (-25)      /* a padded size or plane offset exceeds the range  */
+
+/* device status bits, read with o2m_get_status */
+#define O2M_STATUS_OVERFLOW 1   /* gauss mode: 2k max|A_i| max|B_j| > (M-1)/2    */
+
+#define O2M_MAX_MODULI 22
+#define O2M_MAX_K 149130
+
+/* C = A B, A m x k, B k x n, complex128 (Section 3.2, Algorithm 1). */
+o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                    double *C, int ldc, int n_moduli, void *stream);
+
+/* C = A B in complex64: fp32 inputs are widened exactly, the same algorithm
+   runs, and the result is rounded to fp32 (Section 3.2; accuracy near fp32
+   needs about 8 moduli). */
+o2m_status cgemm_2m(int m, int n, int k, const float *A, int lda, const float *B, int ldb,
+                    float *C, int ldc, int n_moduli, void *stream);
+
+/* HERK, C = A A^H, A n x k complex128 (Section 5): one int8 GEMM per modulus
+   (C+ = A+ A-^T, C- = C+^T).  uplo must be 'L' or 'l': the lower triangle
+   including the diagonal is written, with Im(c_ii) = 0 exactly; the strictly
+   upper triangle of C is not touched. */
+o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
+                    int n_moduli, void *stream);
+
+/* SYRK, C = A A^T, A n x k real fp64 (Section 5): Z = A[:, :k'] + i A[:, k':]
+   with k' = ceil(k/2) (a zero column pads odd k), C = Re(Z Z^H) by the 2M
+   HERK.  uplo 'L' or 'l': lower triangle of the real n x n C written. */
+o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
+                    int n_moduli, void *stream);
+
+/* Exact Gaussian-integer product (Section 2): A m x k and B k x n with int32
+   (re, im) pairs, C m x n with int64 (re, im) pairs.  No scaling: 2M modulo
+   N moduli with N <= 8 (M < 2^63).  Exact when every entry satisfies
+   2k max_p|A_ip| max_p|B_pj| <= (M-1)/2 (max over Re and Im parts);
+   otherwise the device status bit O2M_STATUS_OVERFLOW is set. */
+o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const int32_t *B,
+                         int ldb, int64_t *C, int ldc, int n_moduli, void *stream);
+
+/* Test hook for zgemm_2m: the per-modulus result of the 2M post step
+   (eq. 2m-post), i.e. (Re c_ij mod m_l, Im c_ij mod m_l) of the exact
+   quantized product, in the symmetric range [-(m_l-1)/2, (m_l-1)/2].
+   res is a device int8 array [n_moduli][2][n][m] (column-major m x n planes,
+   Re plane then Im plane per modulus); E, F (device int32, may be NULL)
+   receive the row / column exponents, with INT32_MIN for a non-finite row /
+   column. */
+o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, const double *B,
+                             int ldb, int n_moduli, int8_t *res, int32_t *E, int32_t *F,
+                             void *stream);
+
+/* Host-only: the first n_moduli 2M moduli (Section 4), their smallest square
+   roots of -1 (Section 2) and log2 of their product.  Any pointer may be
+   NULL.  Touches no GPU. */
+o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out);
+
+/* Host-only: the scaling budget P of the scaling rule above for a given
+   n_moduli and inner dimension k. */
+o2m_status o2m_budget(int n_moduli, int k, int *P_out);
+
+/* Bytes of workspace a call needs.  op: 'z' zgemm, 'c' cgemm, 'h' zherk,
+   's' dsyrk, 'g' gauss, 'r' zgemm_2m_residues.  Touches no GPU. */
+size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli);
+
+/* Use caller-owned device memory (on the current device) as the workspace
+   from now on; NULL returns to library-managed memory.  The caller keeps
+   ownership and must keep it alive while calls using it may still run. */
+o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes);
+
+/* Synchronize stream, return the device status bits of the current device
+   in *device_status and clear them. */
+o2m_status o2m_get_status(void *stream, int *device_status);
+
+/* Phase timing for profiling: when enabled, every call records HIP events
+   around its phases (scale, residues, int8 GEMM, CRT) on its stream.
+   o2m_phase_times synchronizes on the last call's events and writes the
+   elapsed milliseconds of up to max_phases phases; returns the count. */
+o2m_status o2m_phase_timing(int enable);
+int o2m_phase_times(float *ms, int max_phases);
+
+/* Human-readable text for a status code. */
+const char *o2m_status_string(o2m_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* O2M_H */

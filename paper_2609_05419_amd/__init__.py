@@ -1,0 +1,231 @@
+"""2M + Ozaki-II complex GEMM / HERK / SYRK on MI355X (gfx950).
+
+Thin ctypes binding over the C-ABI library ``libo2m.so`` (include/o2m.h).
+Every step of the computation runs in the library's HIP kernels; this module
+only marshals torch tensors (device memory and the current stream) into the
+C calls.  There is no fallback: if the library is missing, importing this
+package raises.
+
+Matrices are column-major: a tensor ``A`` of shape (m, k) must have
+``A.stride(0) == 1`` (``colmajor(x)`` makes such a tensor).  Outputs are
+allocated column-major as well.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
+    "moduli", "budget", "workspace_bytes", "set_workspace", "get_status", "phase_timing",
+    "phase_times", "colmajor", "O2MError", "LIB_PATH",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libo2m.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it first (python -c 'import __graft_entry__ as g; g.build()')")
+
+_L = ctypes.CDLL(LIB_PATH)
+_I, _P, _D = ctypes.c_int, ctypes.c_void_p, ctypes.c_double
+_L.zgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.cgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.zherk_2m.argtypes = [ctypes.c_char, _I, _I, _P, _I, _P, _I, _I, _P]
+_L.dsyrk_2m.argtypes = [ctypes.c_char, _I, _I, _P, _I, _P, _I, _I, _P]
+_L.gauss_gemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.zgemm_2m_residues.argtypes = [_I, _I, _I, _P, _I, _P, _I, _I, _P, _P, _P, _P]
+_L.o2m_moduli.argtypes = [_I, _P, _P, _P]
+_L.o2m_budget.argtypes = [_I, _I, _P]
+_L.o2m_workspace_bytes.argtypes = [ctypes.c_char, _I, _I, _I, _I]
+_L.o2m_workspace_bytes.restype = ctypes.c_size_t
+_L.o2m_set_workspace.argtypes = [_P, ctypes.c_size_t]
+_L.o2m_get_status.argtypes = [_P, _P]
+_L.o2m_phase_timing.argtypes = [_I]
+_L.o2m_phase_times.argtypes = [_P, _I]
+_L.o2m_status_string.argtypes = [_I]
+_L.o2m_status_string.restype = ctypes.c_char_p
+for _f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
+           "o2m_moduli", "o2m_budget", "o2m_set_workspace", "o2m_get_status", "o2m_phase_timing",
+           "o2m_phase_times"):
+    getattr(_L, _f).restype = _I
+
+STATUS_OVERFLOW = 1
+
+
+class O2MError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = _L.o2m_status_string(status).decode()
+        super().__init__(f"{where}: status {status} ({msg})")
+        self.status = status
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise O2MError(status, where)
+
+
+def colmajor(x: torch.Tensor) -> torch.Tensor:
+    """Same values, column-major storage (stride(0) == 1)."""
+    return x.t().contiguous().t()
+
+
+def _ld(x: torch.Tensor) -> int:
+    if x.dim() != 2:
+        raise ValueError("expected a matrix")
+    if x.size(0) > 1 and x.stride(0) != 1:
+        raise ValueError("matrix must be column-major (stride(0) == 1); use colmajor()")
+    return max(x.stride(1), x.size(0), 1)
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _empty_colmajor(rows: int, cols: int, dtype, device) -> torch.Tensor:
+    return torch.empty((cols, rows), dtype=dtype, device=device).t()
+
+
+def _check_operands(A, B, dtype):
+    for name, x in (("A", A), ("B", B)):
+        if x.dtype != dtype:
+            raise TypeError(f"{name} must be {dtype}, got {x.dtype}")
+        if not x.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+    if A.size(1) != B.size(0):
+        raise ValueError(f"inner dimensions differ: {tuple(A.shape)} x {tuple(B.shape)}")
+
+
+def zgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
+             stream=None) -> torch.Tensor:
+    """C = A B for complex128 A (m x k), B (k x n) by 2M + Ozaki-II."""
+    _check_operands(A, B, torch.complex128)
+    m, k = A.shape
+    n = B.size(1)
+    C = _empty_colmajor(m, n, torch.complex128, A.device) if out is None else out
+    _check(_L.zgemm_2m(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
+                       n_moduli, _stream(stream)), "zgemm_2m")
+    return C
+
+
+def cgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 8, out: torch.Tensor | None = None,
+             stream=None) -> torch.Tensor:
+    """C = A B for complex64 A, B by 2M + Ozaki-II (result rounded to fp32)."""
+    _check_operands(A, B, torch.complex64)
+    m, k = A.shape
+    n = B.size(1)
+    C = _empty_colmajor(m, n, torch.complex64, A.device) if out is None else out
+    _check(_L.cgemm_2m(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
+                       n_moduli, _stream(stream)), "cgemm_2m")
+    return C
+
+
+def zherk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Lower triangle of C = A A^H (complex128 A, n x k).  The strictly upper
+    triangle of a fresh output is zero-initialised; of ``out`` it is left alone."""
+    if A.dtype != torch.complex128 or not A.is_cuda:
+        raise TypeError("A must be a complex128 device tensor")
+    n, k = A.shape
+    if out is None:
+        out = colmajor(torch.zeros((n, n), dtype=torch.complex128, device=A.device))
+    _check(_L.zherk_2m(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+                       _stream(stream)), "zherk_2m")
+    return out
+
+
+def dsyrk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Lower triangle of C = A A^T (float64 A, n x k) via the half-k 2M HERK."""
+    if A.dtype != torch.float64 or not A.is_cuda:
+        raise TypeError("A must be a float64 device tensor")
+    n, k = A.shape
+    if out is None:
+        out = colmajor(torch.zeros((n, n), dtype=torch.float64, device=A.device))
+    _check(_L.dsyrk_2m(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+                       _stream(stream)), "dsyrk_2m")
+    return out
+
+
+def gauss_gemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 4, out: torch.Tensor | None = None,
+                  stream=None) -> torch.Tensor:
+    """Exact Gaussian-integer product.  A: int32 tensor of shape (m, k, 2) whose
+    storage is column-major complex (stride (2, 2*lda, 1)); likewise B.  The
+    result is int64 of shape (m, n, 2), column-major complex."""
+    def ld3(x):
+        if x.dtype != torch.int32 or x.dim() != 3 or x.size(2) != 2 or x.stride(2) != 1 or x.stride(0) != 2:
+            raise ValueError("expected int32 (rows, cols, 2) with column-major complex storage")
+        return max(x.stride(1) // 2, x.size(0), 1)
+    m, k = A.shape[:2]
+    n = B.size(1)
+    if B.size(0) != k:
+        raise ValueError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((n, m, 2), dtype=torch.int64, device=A.device).transpose(0, 1)
+    _check(_L.gauss_gemm_2m(m, n, k, A.data_ptr(), ld3(A), B.data_ptr(), ld3(B), out.data_ptr(),
+                            max(out.stride(1) // 2, m, 1), n_moduli, _stream(stream)), "gauss_gemm_2m")
+    return out
+
+
+def zgemm_2m_residues(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, stream=None):
+    """Test hook: per-modulus (Re c mod m_l, Im c mod m_l) of the quantized
+    product, int8 [n_moduli, 2, n, m] (symmetric residues), and the row /
+    column exponents E (m,), F (n,)."""
+    _check_operands(A, B, torch.complex128)
+    m, k = A.shape
+    n = B.size(1)
+    res = torch.empty((n_moduli, 2, n, m), dtype=torch.int8, device=A.device)
+    E = torch.empty(m, dtype=torch.int32, device=A.device)
+    F = torch.empty(n, dtype=torch.int32, device=A.device)
+    _check(_L.zgemm_2m_residues(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), n_moduli,
+                                res.data_ptr(), E.data_ptr(), F.data_ptr(), _stream(stream)),
+           "zgemm_2m_residues")
+    return res, E, F
+
+
+def moduli(n_moduli: int):
+    """(moduli, roots of -1, log2 M) of the first n_moduli 2M moduli (host only)."""
+    ms = (ctypes.c_int32 * n_moduli)()
+    ss = (ctypes.c_int32 * n_moduli)()
+    l2 = ctypes.c_double()
+    _check(_L.o2m_moduli(n_moduli, ctypes.addressof(ms), ctypes.addressof(ss), ctypes.addressof(l2)),
+           "o2m_moduli")
+    return list(ms), list(ss), l2.value
+
+
+def budget(n_moduli: int, k: int) -> int:
+    P = ctypes.c_int()
+    _check(_L.o2m_budget(n_moduli, k, ctypes.addressof(P)), "o2m_budget")
+    return P.value
+
+
+def workspace_bytes(op: str, m: int, n: int, k: int, n_moduli: int) -> int:
+    return int(_L.o2m_workspace_bytes(op.encode()[:1], m, n, k, n_moduli))
+
+
+def set_workspace(buf: torch.Tensor | None) -> None:
+    if buf is None:
+        _check(_L.o2m_set_workspace(None, 0), "o2m_set_workspace")
+    else:
+        _check(_L.o2m_set_workspace(buf.data_ptr(), buf.numel() * buf.element_size()), "o2m_set_workspace")
+
+
+def get_status(stream=None) -> int:
+    st = ctypes.c_int()
+    _check(_L.o2m_get_status(_stream(stream), ctypes.addressof(st)), "o2m_get_status")
+    return st.value
+
+
+def phase_timing(enable: bool) -> None:
+    _check(_L.o2m_phase_timing(1 if enable else 0), "o2m_phase_timing")
+
+
+PHASES = ("scale", "residues", "int8_gemm", "crt")
+
+
+def phase_times() -> dict:
+    """Mean milliseconds per phase over the calls since phase_timing(True)."""
+    buf = (ctypes.c_float * 4)()
+    n = _L.o2m_phase_times(ctypes.addressof(buf), 4)
+    if n < 0:
+        raise RuntimeError("o2m_phase_times failed")
+    return {PHASES[i]: float(buf[i]) for i in range(n)}

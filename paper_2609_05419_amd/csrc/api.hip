@@ -1,0 +1,456 @@
+// C-ABI entry points of the 2M + Ozaki-II library (declared in include/o2m.h).
+//
+// Every call validates its arguments on the host, then enqueues on the
+// caller's stream:
+//   K1  per-row / per-column maxima and exponents      (Algorithm 1, step 2)
+//   K2  quantize, residues and 2M pre into int8 planes (steps 3-4, eq. 2m-pre)
+//   K3  batched int8 MFMA GEMMs, C mod m as int8       (step 4, eq. 2m-mul)
+//   K4  2M post, CRT, symmetric lift, descale          (steps 4-7, eq. 2m-post)
+// and returns without synchronizing.
+#include <math.h>
+#include <mutex>
+#include <stdio.h>
+#include <string.h>
+
+#include "o2m.h"
+#include "o2m_internal.h"
+
+using namespace o2m;
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int kPhaseCount = 4;
+constexpr int kMaxTimedCalls = 1024;
+
+struct DeviceState {
+    void *ws = nullptr;      // library-owned workspace
+    size_t ws_bytes = 0;
+    void *user_ws = nullptr; // caller-owned workspace (if set)
+    size_t user_bytes = 0;
+    int *status = nullptr;   // device status word
+};
+
+std::mutex g_mu;
+DeviceState g_dev[kMaxDevices];
+
+// phase timing
+bool g_timing = false;
+hipEvent_t g_events[kMaxTimedCalls][kPhaseCount + 1];
+bool g_events_made[kMaxTimedCalls];
+int g_timed_calls = 0;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Carver {
+    char *base;
+    size_t off = 0;
+    explicit Carver(void *b) : base((char *)b) {}
+    void *take(size_t bytes) {
+        void *p = base ? base + off : nullptr;
+        off += align256(bytes);
+        return p;
+    }
+};
+
+int floor_half(int P) { return P >= 0 ? P / 2 : -((-P + 1) / 2); }
+
+// Geometry of one call
+struct Geometry {
+    int rows_a, rows_b;       // operand rows (m and n; HERK/SYRK: n and n)
+    int k;                    // logical inner dimension
+    int a_pad, b_pad, kpad, kblocks;
+    size_t plane_a, plane_b, plane_c;
+    int products;             // 2N (GEMM) or N (HERK/SYRK)
+    bool shared_planes;       // HERK/SYRK: B planes are the A- planes
+};
+
+Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym) {
+    Geometry g;
+    g.rows_a = rows_a;
+    g.rows_b = rows_b;
+    g.k = k;
+    g.a_pad = round_up(rows_a > 0 ? rows_a : 1, kRowBlock);
+    g.b_pad = round_up(rows_b > 0 ? rows_b : 1, kRowBlock);
+    g.kpad = round_up(k > 0 ? k : 1, kStageK);
+    g.kblocks = g.kpad / kStageK;
+    g.plane_a = (size_t)g.a_pad * g.kpad;
+    g.plane_b = (size_t)g.b_pad * g.kpad;
+    g.plane_c = (size_t)g.a_pad * g.b_pad;
+    g.products = sym ? N : 2 * N;
+    g.shared_planes = sym;
+    return g;
+}
+
+struct Buffers {
+    unsigned long long *amax_a, *amax_b;
+    int32_t *E, *F;
+    int8_t *planes_a, *planes_b, *res;
+};
+
+size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
+    Carver c(base);
+    Buffers t;
+    t.amax_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
+    t.amax_b = g.shared_planes ? t.amax_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
+    t.E = (int32_t *)c.take(sizeof(int32_t) * g.a_pad);
+    t.F = g.shared_planes ? t.E : (int32_t *)c.take(sizeof(int32_t) * g.b_pad);
+    t.planes_a = (int8_t *)c.take(g.plane_a * 2 * N);
+    t.planes_b = g.shared_planes ? t.planes_a : (int8_t *)c.take(g.plane_b * 2 * N);
+    t.res = (int8_t *)c.take(g.plane_c * g.products);
+    if (b) *b = t;
+    return c.off;
+}
+
+o2m_status hip_fail(hipError_t e) {
+    if (e == hipSuccess) return O2M_OK;
+    if (getenv("O2M_LOG")) fprintf(stderr, "o2m: HIP error %d (%s)\n", (int)e, hipGetErrorString(e));
+    return O2M_ERR_HIP;
+}
+
+#define O2M_TRY(expr)                                        \
+    do {                                                     \
+        hipError_t e_ = (expr);                              \
+        if (e_ != hipSuccess) return hip_fail(e_);           \
+    } while (0)
+
+// Returns a device buffer of at least `bytes` on the current device.
+o2m_status workspace(size_t bytes, void **out, int **status) {
+    int dev = 0;
+    O2M_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_mu);
+    DeviceState &d = g_dev[dev];
+    if (!d.status) {
+        O2M_TRY(hipMalloc((void **)&d.status, 256));
+        O2M_TRY(launch_zero(d.status, 256, nullptr));
+        O2M_TRY(hipDeviceSynchronize());
+    }
+    *status = d.status;
+    if (d.user_ws) {
+        if (d.user_bytes < bytes) return O2M_ERR_WORKSPACE;
+        *out = d.user_ws;
+        return O2M_OK;
+    }
+    if (d.ws_bytes < bytes) {
+        // in-flight calls on any stream may still use the old buffer
+        O2M_TRY(hipDeviceSynchronize());
+        if (d.ws) O2M_TRY(hipFree(d.ws));
+        d.ws = nullptr;
+        d.ws_bytes = 0;
+        if (hipMalloc(&d.ws, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            d.ws = nullptr;
+            return O2M_ERR_NOMEM;
+        }
+        d.ws_bytes = bytes;
+    }
+    *out = d.ws;
+    return O2M_OK;
+}
+
+int g_call_slot = -1;
+
+void phase_mark(int phase, hipStream_t st) {
+    if (!g_timing) return;
+    if (phase == 0) {
+        if (g_timed_calls >= kMaxTimedCalls) { g_call_slot = -1; return; }
+        g_call_slot = g_timed_calls++;
+        if (!g_events_made[g_call_slot]) {
+            for (int p = 0; p <= kPhaseCount; ++p) (void)hipEventCreate(&g_events[g_call_slot][p]);
+            g_events_made[g_call_slot] = true;
+        }
+    }
+    if (g_call_slot >= 0) (void)hipEventRecord(g_events[g_call_slot][phase], st);
+}
+
+enum Op { kOpZ, kOpC, kOpH, kOpS, kOpG, kOpR };
+
+struct Call {
+    Op op;
+    int m, n, k;
+    const void *A; int lda;
+    const void *B; int ldb;
+    void *C; int ldc;
+    int N;
+    hipStream_t st;
+    int8_t *res_out;
+    int32_t *E_out, *F_out;
+};
+
+o2m_status run(const Call &c) {
+    const bool sym = c.op == kOpH || c.op == kOpS;
+    const int kc = c.op == kOpS ? (c.k + 1) / 2 : c.k;
+    const ModuliTable *t = moduli_table(c.N);
+    if (!t) return O2M_ERR_NMODULI;
+    const Geometry g = make_geometry(c.m, sym ? c.m : c.n, kc, c.N, sym);
+    if ((long)g.a_pad * g.b_pad > (1L << 40) || (long)g.a_pad / kRowBlock * (g.b_pad / kRowBlock) * g.products > 0x7FFFFFFFL)
+        return O2M_ERR_SIZE;
+    void *ws = nullptr;
+    int *status = nullptr;
+    const size_t need = carve(g, c.N, nullptr, nullptr);
+    o2m_status s = workspace(need, &ws, &status);
+    if (s != O2M_OK) return s;
+    Buffers b;
+    carve(g, c.N, ws, &b);
+
+    int pA = 0, pB = 0;
+    if (c.op != kOpG) {
+        const int P = budget(t, kc);
+        pA = floor_half(P);
+        pB = sym ? pA : P - pA;
+    }
+    const ElemType et = c.op == kOpC ? kF32 : c.op == kOpG ? kI32 : c.op == kOpS ? kR64 : kF64;
+
+    phase_mark(0, c.st);
+    // ---- K1: maxima and exponents ------------------------------------------
+    O2M_TRY(launch_zero(b.amax_a, sizeof(unsigned long long) * g.a_pad, c.st));
+    O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
+    if (!sym) {
+        O2M_TRY(launch_zero(b.amax_b, sizeof(unsigned long long) * g.b_pad, c.st));
+        O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
+    }
+    if (c.op != kOpG) {
+        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, c.st));
+        if (!sym) O2M_TRY(launch_exponents(c.n, b.amax_b, b.F, c.st));
+    }
+    phase_mark(1, c.st);
+
+    // ---- K2: residues + 2M pre ---------------------------------------------
+    PlaneGeom ga = {c.m, kc, c.k, g.a_pad, g.kblocks, g.plane_a};
+    if (c.op == kOpS) {
+        O2M_TRY(launch_residues(2, kR64, c.A, c.lda, b.E, pA, kc, ga, t->res, b.planes_a, c.st));
+    } else {
+        O2M_TRY(launch_residues(0, et, c.A, c.lda, c.op == kOpG ? nullptr : b.E, pA, 0, ga, t->res,
+                                b.planes_a, c.st));
+    }
+    if (!sym) {
+        PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, g.kblocks, g.plane_b};
+        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, 0, gb, t->res,
+                                b.planes_b, c.st));
+    }
+    phase_mark(2, c.st);
+
+    // ---- K3: int8 GEMMs ----------------------------------------------------
+    GemmArgs gm;
+    memset(&gm, 0, sizeof gm);
+    gm.a = b.planes_a;
+    gm.b = sym ? b.planes_a + g.plane_a : b.planes_b;
+    gm.c = b.res;
+    gm.a_pstride = sym ? 2 * g.plane_a : g.plane_a;
+    gm.b_pstride = sym ? 2 * g.plane_a : g.plane_b;
+    gm.c_pstride = g.plane_c;
+    gm.mt = g.a_pad / kRowBlock;
+    gm.nt = g.b_pad / kRowBlock;
+    gm.kblocks = g.kblocks;
+    gm.batch = g.products;
+    gm.mod_shift = sym ? 0 : 1;
+    gm.ldc = g.a_pad;
+    for (int l = 0; l < c.N; ++l) { gm.mod[l] = t->res.mod[l]; gm.inv[l] = t->res.inv[l]; }
+    O2M_TRY(launch_gemm(gm, c.st));
+    phase_mark(3, c.st);
+
+    // ---- K4: 2M post + CRT + lift + descale ---------------------------------
+    CrtArgs ca;
+    memset(&ca, 0, sizeof ca);
+    ca.res = b.res;
+    ca.plane_bytes = g.plane_c;
+    ca.ldr = g.a_pad;
+    ca.m = c.m;
+    ca.n = sym ? c.m : c.n;
+    ca.c = c.op == kOpR ? (void *)c.res_out : c.C;
+    ca.ldc = c.ldc;
+    ca.E = b.E;
+    ca.F = sym ? b.E : b.F;
+    ca.scale_bias = -(pA + pB);
+    ca.amaxA = b.amax_a;
+    ca.amaxB = b.amax_b;
+    ca.k = c.k;
+    ca.status = status;
+    ca.rp = t->res;
+    int mode = 0;
+    ElemType ot = kF64;
+    switch (c.op) {
+    case kOpZ: mode = 0; break;
+    case kOpC: mode = 0; ot = kF32; break;
+    case kOpH: mode = 1; break;
+    case kOpS: mode = 2; break;
+    case kOpG: mode = 3; break;
+    case kOpR: mode = 4; break;
+    }
+    O2M_TRY(launch_crt(mode, ot, ca, t->crt, c.st));
+    if (c.op == kOpR) {
+        if (c.E_out) O2M_TRY(hipMemcpyAsync(c.E_out, b.E, sizeof(int32_t) * c.m, hipMemcpyDeviceToDevice, c.st));
+        if (c.F_out) O2M_TRY(hipMemcpyAsync(c.F_out, b.F, sizeof(int32_t) * c.n, hipMemcpyDeviceToDevice, c.st));
+    }
+    phase_mark(4, c.st);
+    if (getenv("O2M_LOG"))
+        fprintf(stderr, "o2m: op=%d m=%d n=%d k=%d N=%d log2M=%.2f pA=%d pB=%d T=%d ws=%zu\n", (int)c.op,
+                c.m, c.n, c.k, c.N, t->log2M, pA, pB, t->crt.limbs, need);
+    return O2M_OK;
+}
+
+// BLAS-style argument checks shared by the GEMM-shaped calls
+o2m_status check_gemm(int m, int n, int k, const void *A, int lda, const void *B, int ldb, const void *C,
+                      int ldc, int N, int maxN) {
+    if (m < 0) return -1;
+    if (n < 0) return -2;
+    if (k < 0) return -3;
+    if (!A && m > 0 && k > 0) return -4;
+    if (lda < (m > 1 ? m : 1)) return -5;
+    if (!B && k > 0 && n > 0) return -6;
+    if (ldb < (k > 1 ? k : 1)) return -7;
+    if (!C && m > 0 && n > 0) return -8;
+    if (ldc < (m > 1 ? m : 1)) return -9;
+    if (N < 1 || N > maxN) return O2M_ERR_NMODULI;
+    if (k > O2M_MAX_K) return O2M_ERR_KLIMIT;
+    return O2M_OK;
+}
+
+o2m_status check_sym(char uplo, int n, int k, const void *A, int lda, const void *C, int ldc, int N) {
+    if (uplo != 'L' && uplo != 'l') return -1;
+    if (n < 0) return -2;
+    if (k < 0) return -3;
+    if (!A && n > 0 && k > 0) return -4;
+    if (lda < (n > 1 ? n : 1)) return -5;
+    if (!C && n > 0) return -6;
+    if (ldc < (n > 1 ? n : 1)) return -7;
+    if (N < 1 || N > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (k > O2M_MAX_K) return O2M_ERR_KLIMIT;
+    return O2M_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                    int ldc, int n_moduli, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+}
+
+o2m_status cgemm_2m(int m, int n, int k, const float *A, int lda, const float *B, int ldb, float *C,
+                    int ldc, int n_moduli, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpC, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+}
+
+o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
+                    void *stream) {
+    o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
+    if (s != O2M_OK || n == 0) return s;
+    return run(Call{kOpH, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+}
+
+o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
+                    void *stream) {
+    o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
+    if (s != O2M_OK || n == 0) return s;
+    return run(Call{kOpS, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+}
+
+o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const int32_t *B, int ldb,
+                         int64_t *C, int ldc, int n_moduli, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, 8);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpG, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+}
+
+o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                             int n_moduli, int8_t *res, int32_t *E, int32_t *F, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, res, m > 1 ? m : 1, n_moduli, O2M_MAX_MODULI);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpR, m, n, k, A, lda, B, ldb, nullptr, m, n_moduli, (hipStream_t)stream, res, E, F});
+}
+
+o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out) {
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    const ModuliTable *t = moduli_table(n_moduli);
+    for (int l = 0; l < n_moduli; ++l) {
+        if (m_out) m_out[l] = t->res.mod[l];
+        if (s_out) s_out[l] = t->res.root[l];
+    }
+    if (log2M_out) *log2M_out = t->log2M;
+    return O2M_OK;
+}
+
+o2m_status o2m_budget(int n_moduli, int k, int *P_out) {
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (k < 0) return -2;
+    if (!P_out) return -3;
+    *P_out = budget(moduli_table(n_moduli), k);
+    return O2M_OK;
+}
+
+size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli) {
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI || m < 0 || n < 0 || k < 0) return 0;
+    const bool sym = op == 'h' || op == 's';
+    const int kc = op == 's' ? (k + 1) / 2 : k;
+    const Geometry g = make_geometry(m, sym ? m : n, kc, n_moduli, sym);
+    return carve(g, n_moduli, nullptr, nullptr);
+}
+
+o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_dev[dev].user_ws = dev_ptr;
+    g_dev[dev].user_bytes = dev_ptr ? bytes : 0;
+    return O2M_OK;
+}
+
+o2m_status o2m_get_status(void *stream, int *device_status) {
+    if (!device_status) return -2;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
+    hipStream_t st = (hipStream_t)stream;
+    if (hipStreamSynchronize(st) != hipSuccess) return O2M_ERR_HIP;
+    int *p = g_dev[dev].status;
+    if (!p) { *device_status = 0; return O2M_OK; }
+    if (hipMemcpy(device_status, p, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess) return O2M_ERR_HIP;
+    if (launch_zero(p, 256, st) != hipSuccess) return O2M_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return O2M_ERR_HIP;
+    return O2M_OK;
+}
+
+o2m_status o2m_phase_timing(int enable) {
+    g_timing = enable != 0;
+    g_timed_calls = 0;
+    g_call_slot = -1;
+    return O2M_OK;
+}
+
+int o2m_phase_times(float *ms, int max_phases) {
+    const int n = g_timed_calls;
+    int count = kPhaseCount < max_phases ? kPhaseCount : max_phases;
+    for (int p = 0; p < count; ++p) ms[p] = 0.0f;
+    if (n == 0) return 0;
+    if (hipEventSynchronize(g_events[n - 1][kPhaseCount]) != hipSuccess) return -1;
+    for (int c = 0; c < n; ++c)
+        for (int p = 0; p < count; ++p) {
+            float t = 0.0f;
+            if (hipEventElapsedTime(&t, g_events[c][p], g_events[c][p + 1]) != hipSuccess) return -1;
+            ms[p] += t / (float)n;
+        }
+    return count;
+}
+
+const char *o2m_status_string(o2m_status s) {
+    switch (s) {
+    case O2M_OK: return "success";
+    case O2M_ERR_NMODULI: return "n_moduli out of range (1..22; gauss mode 1..8)";
+    case O2M_ERR_KLIMIT: return "k exceeds 149130 (int32 accumulation bound)";
+    case O2M_ERR_WORKSPACE: return "caller workspace too small";
+    case O2M_ERR_HIP: return "HIP runtime error";
+    case O2M_ERR_NOMEM: return "workspace allocation failed";
+    case O2M_ERR_SIZE: return "problem too large for the tile grid";
+    default: break;
+    }
+    if (s < 0 && s >= -12) return "invalid argument (BLAS position = -status)";
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,166 @@
+// K1: scaling exponents (Algorithm 1, step 2).
+//
+// The row scale of A and the column scale of B are powers of two,
+// sigma_i = 2^(E_i - pA), tau_j = 2^(F_j - pB), with E_i the frexp exponent
+// of the largest |Re| or |Im| in row i (so that max < 2^E_i).  The maxima are
+// found with atomicMax on the bit patterns of |x| (for non-negative doubles
+// the bit pattern is monotone in the value, and Inf/NaN patterns sit above
+// every finite one, which flags non-finite rows for free).
+//
+// Bound: HBM.  Algorithmic bytes = the matrix read once (16 B per complex
+// fp64 element).  Rows of a column-major A are strided, so a thread owns one
+// row and walks a chunk of columns: every load instruction of a wave reads 64
+// consecutive rows (1 KB contiguous).  Columns of B are contiguous: a block
+// owns a chunk of one column.
+#include "o2m_internal.h"
+
+namespace o2m {
+namespace {
+
+__device__ inline unsigned long long bits_of(double x) {
+    // |x| as a bit pattern: monotone in |x| for finite values, and every NaN
+    // (of either sign) sorts above +Inf once the sign bit is cleared
+    return (unsigned long long)__double_as_longlong(x) & 0x7FFFFFFFFFFFFFFFull;
+}
+
+__device__ inline unsigned long long umax(unsigned long long a, unsigned long long b) { return a > b ? a : b; }
+
+// Bit pattern of max(|Re|, |Im|) of one entry; a NaN in either part wins
+// (fmax would drop it).
+template <ElemType ET> struct Elem;
+template <> struct Elem<kF64> {
+    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
+        const double2 v = reinterpret_cast<const double2 *>(X)[idx];
+        return umax(bits_of(v.x), bits_of(v.y));
+    }
+};
+template <> struct Elem<kF32> {
+    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
+        const float2 v = reinterpret_cast<const float2 *>(X)[idx];
+        return umax(bits_of((double)v.x), bits_of((double)v.y));
+    }
+};
+template <> struct Elem<kI32> {
+    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
+        const int2 v = reinterpret_cast<const int2 *>(X)[idx];
+        return umax(bits_of((double)v.x), bits_of((double)v.y));
+    }
+};
+template <> struct Elem<kR64> {
+    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
+        return bits_of(reinterpret_cast<const double *>(X)[idx]);
+    }
+};
+
+constexpr int kRowChunk = 64;     // columns per thread in row mode
+constexpr int kColChunk = 2048;   // rows per block in column mode
+
+template <ElemType ET>
+__global__ __launch_bounds__(256) void amax_rows(int rows, int cols, const void *X, int ld,
+                                                 unsigned long long *amax) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= rows) return;
+    const int c0 = blockIdx.y * kRowChunk;
+    const int c1 = min(cols, c0 + kRowChunk);
+    unsigned long long best = 0;
+    for (int c = c0; c < c1; ++c) {
+        unsigned long long b = Elem<ET>::bits(X, (size_t)r + (size_t)c * ld);
+        best = b > best ? b : best;
+    }
+    if (best) atomicMax(amax + r, best);
+}
+
+template <ElemType ET>
+__global__ __launch_bounds__(256) void amax_cols(int rows, int cols, const void *X, int ld,
+                                                 unsigned long long *amax) {
+    const int c = blockIdx.x;
+    const int r0 = blockIdx.y * kColChunk;
+    const int r1 = min(rows, r0 + kColChunk);
+    unsigned long long best = 0;
+    for (int r = r0 + threadIdx.x; r < r1; r += 256) {
+        unsigned long long b = Elem<ET>::bits(X, (size_t)r + (size_t)c * ld);
+        best = b > best ? b : best;
+    }
+    // wave reduction, then one atomic per wave
+    for (int off = 32; off > 0; off >>= 1) {
+        unsigned long long o = __shfl_xor(best, off, 64);
+        best = o > best ? o : best;
+    }
+    if ((threadIdx.x & 63) == 0 && best) atomicMax(amax + c, best);
+}
+
+__global__ void exponents_kernel(int count, const unsigned long long *amax, int32_t *E) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= count) return;
+    const unsigned long long b = amax[i];
+    int e;
+    if (b >= 0x7FF0000000000000ull) e = INT32_MIN;      // Inf or NaN in the row
+    else if (b == 0) e = 0;                                // zero row: E = 0
+    else frexp(__longlong_as_double((long long)b), &e);    // max < 2^e
+    E[i] = e;
+}
+
+__global__ void zero_kernel(uint4 *p, size_t n16, unsigned char *tail, int ntail) {
+    size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t stride = (size_t)gridDim.x * 256;
+    for (; i < n16; i += stride) p[i] = make_uint4(0, 0, 0, 0);
+    if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = 0;
+}
+
+__global__ void zero_matrix_kernel(unsigned char *c, int rows_bytes, int n, size_t ld_bytes) {
+    const int j = blockIdx.y;
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < rows_bytes; i += gridDim.x * 256)
+        c[(size_t)j * ld_bytes + i] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X, int ld,
+                       unsigned long long *amax, hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    if (mode == 0) {
+        dim3 grid((rows + 255) / 256, (cols + kRowChunk - 1) / kRowChunk);
+        switch (et) {
+        case kF64: amax_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kF32: amax_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kI32: amax_rows<kI32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kR64: amax_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        }
+    } else {
+        dim3 grid(cols, (rows + kColChunk - 1) / kColChunk);
+        switch (et) {
+        case kF64: amax_cols<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kF32: amax_cols<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kI32: amax_cols<kI32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kR64: amax_cols<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(count, amax, E);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t st) {
+    if (bytes == 0) return hipSuccess;
+    const size_t n16 = bytes / 16;
+    const int ntail = (int)(bytes % 16);
+    size_t blocks = (n16 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks == 0) blocks = 1;
+    zero_kernel<<<(unsigned)blocks, 256, 0, st>>>((uint4 *)p, n16, (unsigned char *)p + n16 * 16, ntail);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_matrix(void *c, int m, int n, int ldc, int elem_bytes, hipStream_t st) {
+    if (m <= 0 || n <= 0) return hipSuccess;
+    const int rows_bytes = m * elem_bytes;
+    dim3 grid((rows_bytes + 255) / 256 < 64 ? (rows_bytes + 255) / 256 : 64, n);
+    zero_matrix_kernel<<<grid, 256, 0, st>>>((unsigned char *)c, rows_bytes, n, (size_t)ldc * elem_bytes);
+    return hipGetLastError();
+}
+
+}  // namespace o2m

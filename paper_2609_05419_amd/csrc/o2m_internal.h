@@ -1,0 +1,172 @@
+// Internal definitions shared by the HIP kernels and the host side of the
+// 2M + Ozaki-II library.  Not part of the public C-ABI (include/o2m.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace o2m {
+
+constexpr int kMaxModuli = 22;
+constexpr int kMaxLimbs = 4;
+constexpr int kLimbBits = 40;  // CRT limb base 2^40: limb sums stay below 2^53
+constexpr int kStatusOverflow = 1;  // device status bit: gauss-mode bound violated
+
+// ---------------------------------------------------------------------------
+// Operand plane layout (the int8 residue planes A+-, B+- of eq. 2m-pre)
+//
+// Every operand plane is R_pad x K_pad int8 values, "K-major": the row index
+// is a row of A (or a column of B) and k runs inside.  It is stored in the
+// order the int8 GEMM consumes it, so that one wave reads one MFMA fragment as
+// a single contiguous 1 KB and one thread block reads one pipeline stage as a
+// single contiguous 32 KB:
+//
+//   block of 256 rows x 64 k       = one GEMM stage for one operand (16 KB)
+//   fragment of 32 rows x 32 k     = one v_mfma_i32_32x32x32_i8 operand (1 KB)
+//   lane chunk of 1 row x 16 k     = 16 bytes held by one lane
+//
+// offset(r, kk) = ((rb*KB + kb)*16 + ks*8 + rg)*1024 + lane*16 + (kk & 15)
+// with rb = r/256, rg = (r%256)/32, kb = kk/64, ks = (kk%64)/32,
+// lane = (r%32) + 32*((kk%32)/16), KB = K_pad/64.
+// ---------------------------------------------------------------------------
+constexpr int kRowBlock = 256;
+constexpr int kStageK = 64;
+constexpr int kFragBytes = 1024;
+constexpr int kStageBytes = kRowBlock * kStageK;  // 16 KB per operand per stage
+
+__host__ __device__ inline size_t plane_offset(int r, int kk, int kblocks) {
+    const int rb = r >> 8, rr = r & 255;
+    const int kb = kk >> 6, kr = kk & 63;
+    const int rg = rr >> 5, ks = kr >> 5;
+    const int lane = (rr & 31) + (((kr & 31) >> 4) << 5);
+    return ((size_t)(rb * kblocks + kb) * 16 + ks * 8 + rg) * kFragBytes + lane * 16 + (kr & 15);
+}
+
+inline int round_up(int x, int q) { return (x + q - 1) / q * q; }
+
+// ---------------------------------------------------------------------------
+// Per-call constants
+// ---------------------------------------------------------------------------
+
+// Residue step (eq. 2m-pre): per modulus m, its root s, fl(1/m) and the
+// symmetric residues of 2^26 and 2^52 used to reduce a quantized integer
+// x = x2 2^52 + x1 2^26 + x0 without integer division.
+struct ResidueParams {
+    int n;                       // number of moduli N
+    int mod[kMaxModuli];
+    int root[kMaxModuli];
+    double inv[kMaxModuli];
+    double c26[kMaxModuli];
+    double c52[kMaxModuli];
+};
+
+// CRT step (eq. 2m-post folded into Algorithm 1 step 5): X_re = sum_l u_l W^re_l,
+// X_im = sum_l v_l W^im_l with u = C- + C+, v = C- - C+ and
+// W^re_l = (M/m_l) * [((M/m_l)^-1 2^-1) mod m_l],
+// W^im_l = (M/m_l) * [((M/m_l)^-1 s_l 2^-1) mod m_l], as T balanced limbs.
+struct CrtParams {
+    int n;                        // N
+    int limbs;                    // T
+    double wre[kMaxModuli][kMaxLimbs];
+    double wim[kMaxModuli][kMaxLimbs];
+    double mlimb[kMaxLimbs];      // M in balanced limbs
+    double inv_m;                 // fl(1/M)
+    uint64_t m_lo, m_hi;          // M (gauss mode: M < 2^63, m_hi = 0)
+    uint64_t h_lo;                // (M-1)/2 when M < 2^64 (gauss mode)
+};
+
+// Host-side tables for one N (built once, cached).
+struct ModuliTable {
+    int n;
+    double log2M;
+    ResidueParams res;
+    CrtParams crt;
+    // exact M as 32-bit words (little endian), for the budget computation
+    uint32_t mwords[8];
+    int mwords_len;
+};
+
+// Returns the table for n moduli (1..kMaxModuli), building it on first use.
+const ModuliTable *moduli_table(int n);
+// The 2M moduli in greedy order (Section 4); returns the count (22).
+int moduli_2m(int *out, int cap);
+// Smallest s with s^2 = -1 mod m, or 0 if none.
+int root_of_minus_one(int m);
+// Largest P with 2k 2^P <= (M-1)/2 - floor(M/2^32).
+int budget(const ModuliTable *t, int k);
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (each .hip file exports its own)
+// ---------------------------------------------------------------------------
+
+enum ElemType { kF64 = 0, kF32 = 1, kI32 = 2, kR64 = 3 /* real fp64 */ };
+
+// K1: max |Re|,|Im| per row (mode 0) or per column (mode 1) of a column-major
+// matrix, into amax bits (uint64, atomicMax of |x| bit patterns).
+hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X, int ld,
+                       unsigned long long *amax, hipStream_t st);
+// K1 finish: amax bits -> exponents (INT32_MIN when non-finite).
+hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st);
+
+// K2: quantize + residues + 2M pre into operand planes.
+//   mode 0: operand rows are rows of X (A, m x k), element (r, kk) at X[r + kk*ld]
+//   mode 1: operand rows are columns of X (B, k x n), element (r, kk) at X[kk + r*ld]
+//   mode 2: SYRK, X real n x k, element (r, kk) = X[r + kk*ld] + i X[r + (kk+kh)*ld]
+//   shift: quantization shift p (value scaled by 2^(p - E_r)); E may be NULL (gauss).
+struct PlaneGeom {
+    int rows, k;         // logical sizes (SYRK: k = ceil(kreal / 2))
+    int kreal;           // SYRK: columns of the real matrix
+    int rows_pad, kblocks;
+    size_t plane_bytes;  // rows_pad * kblocks * 64
+};
+hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
+                           int khalf, const PlaneGeom &g, const ResidueParams &rp, int8_t *planes,
+                           hipStream_t st);
+
+// K3: batched int8 GEMM  C_p = A_p B_p^T  (both operands K-major planes), then
+// C_p mod m_(p >> mod_shift) stored as int8 (symmetric residue), column-major
+// with leading dimension ldc = m_pad, plane stride ldc * n_pad.
+struct GemmArgs {
+    const int8_t *a;
+    const int8_t *b;
+    int8_t *c;
+    size_t a_pstride, b_pstride, c_pstride;  // bytes between consecutive batch items
+    int mt, nt, kblocks;                     // tiles along m, n; k stages
+    int batch;
+    int mod_shift;
+    int ldc;
+    int mod[kMaxModuli];
+    double inv[kMaxModuli];
+};
+hipError_t launch_gemm(const GemmArgs &ga, hipStream_t st);
+
+// K4: CRT + lift + descale.
+//   mode 0 ZGEMM  (planes 2l = C+, 2l+1 = C-), output complex
+//   mode 1 HERK   (plane l = C+, C- = C+^T), lower triangle, complex
+//   mode 2 SYRK   (as HERK, real part only)
+//   mode 3 gauss  (as ZGEMM, exact int64 output, status bit on overflow)
+//   mode 4 residues hook (as ZGEMM, per-modulus 2M post output)
+struct CrtArgs {
+    const int8_t *res;
+    size_t plane_bytes;
+    int ldr;            // leading dimension of residue planes (m_pad)
+    int m, n;
+    void *c;
+    int ldc;
+    const int32_t *E, *F;
+    int scale_bias;     // -(pA + pB)
+    const unsigned long long *amaxA, *amaxB;  // gauss mode bound check
+    int k;
+    int *status;
+    ResidueParams rp;   // hook mode
+};
+hipError_t launch_crt(int mode, ElemType out_type, const CrtArgs &ca, const CrtParams &cp,
+                      hipStream_t st);
+
+// Utility: zero a device buffer with a fill kernel (safe under graph capture).
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t st);
+// Utility: zero an m x n column-major matrix of elem_bytes elements.
+hipError_t launch_zero_matrix(void *c, int m, int n, int ldc, int elem_bytes, hipStream_t st);
+
+}  // namespace o2m

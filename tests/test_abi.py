@@ -1,0 +1,105 @@
+"""The C-ABI library loads, exports every symbol include/o2m.h declares, and
+its host-only parts (tables, budget, workspace sizes, argument checks) agree
+with the oracle and the header (no GPU: no compute call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "o2m.h")
+LIB = os.path.join(ROOT, "paper_2609_05419_amd", "libo2m.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:o2m_status|size_t|int|const char \*)\s*(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.skip("libo2m.so not built")
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
+              "o2m_moduli", "o2m_budget", "o2m_workspace_bytes", "o2m_set_workspace",
+              "o2m_get_status", "o2m_phase_timing", "o2m_phase_times", "o2m_status_string"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_package_binding_loads():
+    import paper_2609_05419_amd as o2m
+    assert os.path.samefile(o2m.LIB_PATH, LIB)
+
+
+def test_moduli_table_matches_oracle():
+    import paper_2609_05419_amd as o2m
+    for n in (1, 4, 8, 16, 22):
+        ms, ss, l2 = o2m.moduli(n)
+        assert ms == O.moduli_2m(n)
+        assert ss == [O.root_of(q) for q in ms]
+        assert abs(l2 - __import__("math").log2(O.product(ms))) < 1e-9
+
+
+def test_budget_matches_oracle():
+    import paper_2609_05419_amd as o2m
+    for n in (1, 2, 3, 4, 5, 8, 12, 16, 17, 20, 22):
+        for k in (0, 1, 2, 7, 64, 1000, 1024, 8192, 16384, 65536, 149130):
+            assert o2m.budget(n, k) == O.budget(O.moduli_2m(n), k), (n, k)
+
+
+def test_workspace_bytes_grow_with_the_problem():
+    import paper_2609_05419_amd as o2m
+    z = o2m.workspace_bytes("z", 8192, 8192, 8192, 16)
+    # planes: 2N (m + n) k + 2N m n bytes, plus exponents
+    assert z >= 32 * (8192 * 8192 * 3)
+    assert z < 32 * (8192 * 8192 * 3) + (1 << 20)
+    h = o2m.workspace_bytes("h", 8192, 8192, 8192, 16)
+    assert h < z
+    s = o2m.workspace_bytes("s", 8192, 8192, 8192, 16)
+    assert s < h
+    assert o2m.workspace_bytes("z", 8192, 8192, 8192, 23) == 0
+
+
+def test_argument_errors_are_reported_before_any_gpu_work(lib):
+    P = ctypes.c_void_p
+    lib.zgemm_2m.argtypes = [ctypes.c_int] * 3 + [P, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int, P]
+    fake = P(0x1000)
+    call = lambda *a: lib.zgemm_2m(*a)
+    assert call(-1, 4, 4, fake, 4, fake, 4, fake, 4, 16, None) == -1
+    assert call(4, -1, 4, fake, 4, fake, 4, fake, 4, 16, None) == -2
+    assert call(4, 4, -1, fake, 4, fake, 4, fake, 4, 16, None) == -3
+    assert call(4, 4, 4, None, 4, fake, 4, fake, 4, 16, None) == -4
+    assert call(4, 4, 4, fake, 3, fake, 4, fake, 4, 16, None) == -5
+    assert call(4, 4, 4, fake, 4, None, 4, fake, 4, 16, None) == -6
+    assert call(4, 4, 4, fake, 4, fake, 3, fake, 4, 16, None) == -7
+    assert call(4, 4, 4, fake, 4, fake, 4, None, 4, 16, None) == -8
+    assert call(4, 4, 4, fake, 4, fake, 4, fake, 3, 16, None) == -9
+    assert call(4, 4, 4, fake, 4, fake, 4, fake, 4, 0, None) == -20
+    assert call(4, 4, 4, fake, 4, fake, 4, fake, 4, 23, None) == -20
+    assert call(4, 4, 149131, fake, 4, fake, 149131, fake, 4, 16, None) == -21
+    # empty outputs are a no-op that touches nothing
+    assert call(0, 4, 4, None, 1, fake, 4, fake, 1, 16, None) == 0
+    assert call(4, 0, 4, fake, 4, fake, 4, None, 4, 16, None) == 0
+    lib.gauss_gemm_2m.argtypes = lib.zgemm_2m.argtypes
+    assert lib.gauss_gemm_2m(4, 4, 4, fake, 4, fake, 4, fake, 4, 9, None) == -20
+    lib.zherk_2m.argtypes = [ctypes.c_char, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int, P]
+    assert lib.zherk_2m(b"U", 4, 4, fake, 4, fake, 4, 16, None) == -1
+    assert lib.zherk_2m(b"L", 4, 4, fake, 3, fake, 4, 16, None) == -5
+    assert lib.zherk_2m(b"L", 0, 4, None, 1, None, 1, 16, None) == 0
+    lib.o2m_status_string.restype = ctypes.c_char_p
+    assert b"n_moduli" in lib.o2m_status_string(-20)

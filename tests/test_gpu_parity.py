@@ -1,0 +1,298 @@
+"""Parity of the HIP path (through the C-ABI) with the CPU oracle.
+
+Floating-point results are compared bit for bit with the oracle's exact output
+of Algorithm 1 (the quantized product, rounded to nearest fp64, rescaled):
+the GPU path computes that same number exactly, so any difference is a bug.
+Accuracy against the unquantized product (double-double reference) is checked
+separately with the tolerance 4 u k |A||B| (u = 2^-53 for ZGEMM, 2^-24 for
+CGEMM)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from conftest import same_bits
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def o2m():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_05419_amd as lib
+    return lib
+
+
+DEV = "cuda:0"
+
+
+def to_dev(x):
+    """Host array (any order) -> device tensor with column-major storage."""
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(x).T)).to(DEV).t()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return np.asfortranarray(t.cpu().numpy())
+
+
+def report(name, **kw):
+    print(f"[parity] {name} " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+# ------------------------------------------------------------------ gauss mode
+
+
+def test_gauss_config1_bit_exact(o2m):
+    sa, sb = W.config_seeds(1)
+    A = W.gauss_matrix(64, 64, sa)
+    B = W.gauss_matrix(64, 64, sb)
+    ref = O.gauss_4m(A, B)
+    ms, ss, _ = o2m.moduli(4)
+    assert ms == [241, 233, 229, 221]
+    assert all((s * s + 1) % q == 0 for q, s in zip(ms, ss))
+    dA = torch.from_numpy(A).to(DEV).transpose(0, 1)
+    dB = torch.from_numpy(B).to(DEV).transpose(0, 1)
+    C = o2m.gauss_gemm_2m(dA, dB, n_moduli=4)
+    got = C.transpose(0, 1).cpu().numpy()
+    assert o2m.get_status() == 0
+    report("gauss 64^3 N=4", equal=bool(np.array_equal(got, ref)))
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("shape,N,lo", [((100, 37, 77), 5, -3000), ((1, 1, 1), 1, -5), ((300, 260, 65), 8, -(2 ** 20))])
+def test_gauss_ragged_bit_exact(o2m, shape, N, lo):
+    m, n, k = shape
+    A = W.gauss_matrix(m, k, 11, lo=lo, hi=-lo)
+    B = W.gauss_matrix(k, n, 12, lo=lo, hi=-lo)
+    ref = O.gauss_4m(A, B)
+    C = o2m.gauss_gemm_2m(torch.from_numpy(A).to(DEV).transpose(0, 1),
+                          torch.from_numpy(B).to(DEV).transpose(0, 1), n_moduli=N)
+    got = C.transpose(0, 1).cpu().numpy()
+    status = o2m.get_status()
+    M = O.product(O.moduli_2m(N))
+    need = 2 * k * max(abs(lo), abs(lo)) ** 2
+    if need <= (M - 1) // 2:
+        assert status == 0
+        assert np.array_equal(got, ref)
+    else:
+        assert status & o2m.STATUS_OVERFLOW
+
+
+def test_gauss_overflow_flag(o2m):
+    A = W.gauss_matrix(8, 16, 1, lo=-(2 ** 30), hi=2 ** 30)
+    B = W.gauss_matrix(16, 8, 2, lo=-(2 ** 30), hi=2 ** 30)
+    o2m.gauss_gemm_2m(torch.from_numpy(A).to(DEV).transpose(0, 1),
+                      torch.from_numpy(B).to(DEV).transpose(0, 1), n_moduli=2)
+    assert o2m.get_status() & o2m.STATUS_OVERFLOW
+    assert o2m.get_status() == 0   # cleared by the read
+
+
+# ------------------------------------------------------------------ ZGEMM
+
+
+ZCASES = [
+    # m, n, k, dist, phi, N
+    (64, 64, 64, "normal", 0.5, 16),
+    (100, 77, 130, "phi", 0.5, 16),
+    (257, 300, 200, "phi", 2.0, 16),
+    (33, 290, 65, "normal", 0.5, 1),
+    (128, 64, 513, "uniform", 0.5, 4),
+    (70, 90, 300, "phi", 2.0, 8),
+    (300, 33, 100, "normal", 0.5, 12),
+    (65, 65, 1000, "phi", 0.5, 18),
+    (40, 50, 96, "phi", 2.0, 20),
+    (31, 47, 33, "normal", 0.5, 22),
+    (5, 3, 1, "normal", 0.5, 22),
+]
+
+
+@pytest.mark.parametrize("case", ZCASES, ids=[f"{c[0]}x{c[1]}x{c[2]}-{c[3]}-N{c[5]}" for c in ZCASES])
+def test_zgemm_bit_exact_vs_oracle(o2m, case):
+    m, n, k, dist, phi, N = case
+    a = W.complex_matrix(m, k, 1000 + m, dist=dist, phi=phi)
+    b = W.complex_matrix(k, n, 2000 + n, dist=dist, phi=phi)
+    ref = O.oq_zgemm(a, b, N)
+    C = o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N)
+    got = host(C)
+    ok = same_bits(got, ref)
+    report("zgemm", shape=(m, n, k), N=N, dist=dist, bitexact=ok,
+           mismatches=int(np.sum(got != ref)))
+    assert ok
+
+
+def test_zgemm_edge_cases(o2m):
+    rng = np.random.default_rng(3)
+    m, n, k = 40, 36, 50
+    a = W.complex_matrix(m, k, 31)
+    b = W.complex_matrix(k, n, 32)
+    a[3, :] = 0.0                       # zero row -> zero row of C
+    b[:, 5] = 0.0                       # zero column
+    a[7, :] *= 2.0 ** 900               # huge row
+    a[8, :] *= 2.0 ** -1060             # subnormal row
+    b[:, 9] *= 2.0 ** -600
+    a[10, 4] = np.nan                   # non-finite row
+    b[2, 11] = complex(np.inf, 0)       # non-finite column
+    b[7, 20] = complex(0.5, np.nan)     # NaN in an imaginary part only
+    a[12, :] = 2.0 ** 7                 # entries exactly at a power of two
+    ref = O.oq_zgemm(a, b, 16)
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    assert same_bits(got, ref)
+    assert np.isnan(got[10, :]).all() and np.isnan(got[:, 11]).all() and np.isnan(got[:, 20]).all()
+    assert (got[3, :][~np.isnan(got[3, :])] == 0).all()
+    del rng
+
+
+def test_zgemm_k_zero_and_empty(o2m):
+    a = np.zeros((5, 0), dtype=np.complex128, order="F")
+    b = np.zeros((0, 4), dtype=np.complex128, order="F")
+    A = torch.zeros((0, 5), dtype=torch.complex128, device=DEV).t()
+    B = torch.zeros((4, 0), dtype=torch.complex128, device=DEV).t()
+    out = o2m.colmajor(torch.full((5, 4), 7.0 + 1j, dtype=torch.complex128, device=DEV))
+    o2m.zgemm_2m(A, B, n_moduli=16, out=out)
+    assert (host(out) == 0).all()
+    del a, b
+
+
+def test_zgemm_with_caller_workspace(o2m):
+    a = W.complex_matrix(90, 70, 41)
+    b = W.complex_matrix(70, 60, 42)
+    need = o2m.workspace_bytes("z", 90, 60, 70, 16)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    o2m.set_workspace(ws)
+    try:
+        got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+        with pytest.raises(o2m.O2MError):
+            o2m.zgemm_2m(to_dev(W.complex_matrix(300, 70, 1)), to_dev(b), n_moduli=16)
+    finally:
+        o2m.set_workspace(None)
+    assert same_bits(got, O.oq_zgemm(a, b, 16))
+
+
+def test_residue_hook_matches_exact_integers(o2m):
+    m, n, k, N = 37, 29, 90, 16
+    a = W.complex_matrix(m, k, 51, dist="phi", phi=2.0)
+    b = W.complex_matrix(k, n, 52, dist="phi", phi=2.0)
+    res, E, F = o2m.zgemm_2m_residues(to_dev(a), to_dev(b), n_moduli=N)
+    res = res.cpu().numpy()
+    E0, _, F0, _ = O.exponents(a, b)
+    assert np.array_equal(E.cpu().numpy(), E0) and np.array_equal(F.cpu().numpy(), F0)
+    ms = O.moduli_2m(N)
+    pA, pB = O.split_budget(O.budget(ms, k))
+    ent = [(i, j) for i in range(0, m, 3) for j in range(0, n, 2)]
+    cint = O.oq_cint(a, b, pA, pB, ent)
+    for (i, j), (cr, ci) in zip(ent, cint):
+        for l, q in enumerate(ms):
+            assert int(res[l, 0, j, i]) == O.symmetric_lift(cr, q)
+            assert int(res[l, 1, j, i]) == O.symmetric_lift(ci, q)
+
+
+def test_zgemm_tolerance_vs_double_double(o2m):
+    """Config 2 shape (1024^3, N(0,1)): the error against the unquantized
+    product meets 4 u k |A||B| for N >= 14 and shrinks ~3.7 bits per modulus."""
+    m = n = k = 1024
+    sa, sb = W.config_seeds(2)
+    a = W.complex_matrix(m, k, sa)
+    b = W.complex_matrix(k, n, sb)
+    rng = np.random.default_rng(5)
+    ent = [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 2048), rng.integers(0, n, 2048))]
+    hi, lo = O.dd_gemm(a, b, entries=ent)
+    absab = np.array([np.sum(np.abs(a[i, :]) * np.abs(b[:, j])) for i, j in ent])
+    A, B = to_dev(a), to_dev(b)
+    curve = {}
+    for N in (8, 10, 12, 14, 16, 18, 20):
+        C = host(o2m.zgemm_2m(A, B, n_moduli=N))
+        c = np.array([C[i, j] for i, j in ent])
+        curve[N] = O.error_vs_reference(c, absab, hi, lo, k, 2.0 ** -53)
+        report("zgemm 1024^3 error", N=N, ratio=f"{curve[N]['ratio']:.3g}", maxrel=f"{curve[N]['maxrel']:.3g}")
+    for N in (14, 16, 18, 20):
+        assert curve[N]["ratio"] <= 1.0
+    seq = [curve[N]["maxrel"] for N in (8, 10, 12, 14, 16)]
+    assert all(x > y for x, y in zip(seq, seq[1:]))
+
+
+# ------------------------------------------------------------------ CGEMM
+
+
+@pytest.mark.parametrize("shape,N", [((100, 90, 130), 8), ((257, 31, 300), 6), ((64, 64, 64), 16)])
+def test_cgemm_bit_exact_vs_oracle(o2m, shape, N):
+    m, n, k = shape
+    a = W.complex_matrix(m, k, 61, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(k, n, 62, dist="uniform", dtype=np.complex64)
+    ref = O.oq_cgemm(a, b, N)
+    got = host(o2m.cgemm_2m(to_dev(a), to_dev(b), n_moduli=N))
+    assert same_bits(got, ref)
+
+
+def test_cgemm_tolerance(o2m):
+    m, n, k = 256, 256, 2048
+    a = W.complex_matrix(m, k, 71, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(k, n, 72, dist="uniform", dtype=np.complex64)
+    got = host(o2m.cgemm_2m(to_dev(a), to_dev(b), n_moduli=8)).astype(np.complex128)
+    hi, lo = O.dd_gemm(a.astype(np.complex128), b.astype(np.complex128))
+    absab = np.abs(a.astype(np.complex128)) @ np.abs(b.astype(np.complex128))
+    err = O.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -24)
+    report("cgemm error", ratio=err["ratio"], maxrel=err["maxrel"])
+    assert err["ratio"] <= 1.0
+
+
+# ------------------------------------------------------------------ HERK / SYRK
+
+
+@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((257, 64), 8), ((33, 500), 20), ((1, 3), 16)])
+def test_zherk_bit_exact_lower_triangle(o2m, shape, N):
+    n, k = shape
+    a = W.complex_matrix(n, k, 81 + n, dist="phi", phi=1.0)
+    ref = O.oq_zherk(a, N)
+    sentinel = 3.25 - 1.5j
+    out = o2m.colmajor(torch.full((n, n), sentinel, dtype=torch.complex128, device=DEV))
+    o2m.zherk_2m(to_dev(a), n_moduli=N, out=out)
+    got = host(out)
+    low = np.tril(np.ones((n, n), dtype=bool))
+    assert same_bits(got[low], ref[low])
+    assert (got[~low] == sentinel).all()
+    assert (np.diag(got).imag == 0).all()
+
+
+@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((70, 65), 16), ((257, 1), 8), ((40, 300), 22)])
+def test_dsyrk_bit_exact_lower_triangle(o2m, shape, N):
+    n, k = shape
+    a = W.real_matrix(n, k, 91 + k)
+    ref = O.oq_dsyrk(a, N)
+    out = o2m.colmajor(torch.full((n, n), -7.0, dtype=torch.float64, device=DEV))
+    o2m.dsyrk_2m(to_dev(a), n_moduli=N, out=out)
+    got = host(out)
+    low = np.tril(np.ones((n, n), dtype=bool))
+    assert same_bits(got[low], ref[low])
+    assert (got[~low] == -7.0).all()
+
+
+# ------------------------------------------------------------------ full size, sampled
+
+
+@pytest.mark.slow
+def test_zgemm_8192_sampled_vs_oracle(o2m):
+    """The benchmark workload (8192^3, U(-0.5,0.5) exp(0.5 N(0,1)), N = 16), in
+    the benchmark's launch configuration, on sampled entries."""
+    m = n = k = 8192
+    N = 16
+    sa, sb = W.config_seeds(3)
+    a = W.complex_matrix(m, k, sa, dist="phi", phi=0.5)
+    b = W.complex_matrix(k, n, sb, dist="phi", phi=0.5)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N))
+    rng = np.random.default_rng(8)
+    ent = [(0, 0), (m - 1, n - 1), (m - 1, 0), (0, n - 1)]
+    ent += [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 60), rng.integers(0, n, 60))]
+    ref = O.oq_zgemm(a, b, N, entries=ent)
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, ref)
+    hi, lo = O.dd_gemm(a, b, entries=ent)
+    absab = np.array([np.sum(np.abs(a[i, :]) * np.abs(b[:, j])) for i, j in ent])
+    err = O.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -53)
+    report("zgemm 8192^3 sampled", ratio=err["ratio"], maxrel=err["maxrel"])
+    assert err["ratio"] <= 1.0
