@@ -9,17 +9,17 @@
 // ldc (= m_pad), so the CRT kernel reads 1 byte per product per output entry
 // instead of 4.
 //
-// Tiling for gfx950: a 256 x 256 output tile per workgroup of 4 waves (2 x 2),
-// each wave owning 128 x 128 = 4 x 4 accumulators of v_mfma_i32_32x32x32_i8.
-// A k-stage of 64 is 16 KB per operand, one contiguous chunk of the plane;
-// stages are double-buffered in LDS and prefetched through registers one
-// stage ahead.  Each wave reads its operand fragments with one ds_read_b128
-// per 1 KB fragment (64 lanes x 16 contiguous bytes: no bank conflicts).
-// Workgroups are mapped to tiles XCD-aware: the hardware deals workgroups to
-// the 8 XCDs round-robin, so each XCD is given a contiguous range of tiles,
-// ordered in groups of 8 tile-rows so that the tiles resident on one XCD share
-// A and B stages in its L2.
-//
+// Tiling for gfx950: a 256 x 256 output tile per workgroup of 8 waves (2 per
+// SIMD, 2 x 4), each wave owning 128 x 64 = 8 x 4 accumulators of
+// v_mfma_i32_16x16x64_i8.  On random int8 data this instruction sustains a
+// markedly higher clock than v_mfma_i32_32x32x32_i8 at the same MAC rate, and
+// the second wave per SIMD hides LDS and barrier latency.  A k-stage of 64 is
+// 16 KB per operand, one contiguous chunk of the plane, copied by direct
+// global->LDS loads (global_load_lds_dwordx4, no register staging) into a ring
+// of 4 stages (128 KB of the 160 KB LDS), so loads run 3 stages ahead of the
+// MFMAs.  Each wave reads an operand fragment with one ds_read_b128 (64 lanes
+// x 16 contiguous bytes: no bank conflicts).
+
 // Bound: int8 MFMA.  Algorithmic work per launch = 2 m n k int8 ops per
 // product (counting the padded-free m, n, k of the problem).
 #include "o2m_internal.h"
@@ -28,15 +28,19 @@ namespace o2m {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;                    // 8 waves: 2 per SIMD
+constexpr int kStages = 4;                       // LDS ring of k-stages (32 KB each)
+constexpr int kStageBuf = 2 * kStageBytes;       // A and B of one stage
+constexpr int kLoadsPerStage = 4;                // 16-byte direct loads per thread per stage
 constexpr int kEpiStride = 272;  // bytes per column of the staged 256 x 256 output tile
-constexpr int kPipeBytes = 2 * 2 * kStageBytes;
+constexpr int kPipeBytes = kStages * kStageBuf;
 constexpr int kEpiBytes = 256 * kEpiStride;
 constexpr int kLdsBytes = kPipeBytes > kEpiBytes ? kPipeBytes : kEpiBytes;
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
 constexpr int kGroupRows = 8;
+
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ inline uint32_t lo32(double d) { return (uint32_t)__double2loint(d); }
 
@@ -49,122 +53,189 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
     return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
 }
 
-// Workgroup b (dealt to XCD b % 8) -> logical tile index: XCD x owns the
-// contiguous range starting at x*q + min(x, r) (q = total / 8, r = total % 8).
-__device__ inline int xcd_remap(int b, int total) {
-    const int q = total >> 3, r = total & 7;
+// Tile schedule.  The hardware deals workgroups to the 8 XCDs round-robin
+// (workgroup b -> XCD b % 8, in dispatch order b / 8 within it).  Each batch
+// item (one int8 GEMM) is split into 8 contiguous chunks of its grouped tile
+// order, one per XCD, and all XCDs sweep the batch items in the same order:
+// at any time the whole chip works on one product, whose operand planes
+// (2 x 64 MB at 8192^2) stay resident in the 256 MB Infinity Cache, while the
+// tiles resident on one XCD (8 tile-rows x 4 tile-columns) share their A and
+// B stages in that XCD's L2.  Slots beyond a product's tile count idle.
+struct TileCoord {
+    int p, ti, tj;
+    bool valid;
+};
+__device__ inline TileCoord tile_of(int b, int mt, int nt, int chunk) {
+    TileCoord c;
     const int x = b & 7, slot = b >> 3;
-    return x * q + (x < r ? x : r) + slot;
+    c.p = slot / chunk;
+    const int t = x * chunk + (slot - c.p * chunk);  // index in the product's grouped order
+    c.valid = t < mt * nt;
+    const int group = t / (kGroupRows * nt);
+    const int first = group * kGroupRows;
+    const int gsize = min(mt - first, kGroupRows);
+    const int within = t - group * kGroupRows * nt;
+    c.ti = first + within % gsize;
+    c.tj = within / gsize;
+    return c;
+}
+
+// s_waitcnt on the vector-memory counter only (gfx9 encoding), n <= 63
+template <int N>
+__device__ inline void wait_vm() {
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0xF << 8));
+}
+
+// Keep the machine scheduler from moving instructions across this point: the
+// fragment reads of the next stage must stay ahead of the current MFMAs.
+__device__ inline void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// lgkmcnt(0): all LDS reads of this wave have returned.  At most 8 fragment
+// reads are ever in flight, which the compiler tracks exactly (the counter
+// holds 15), so MFMAs never wait on reads they do not consume.
+__device__ inline void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// Workgroup barrier without a memory fence: the stage data arrives by direct
+// global->LDS loads that each thread has already waited for (vmcnt), and the
+// LDS reads of the stage being recycled have completed (lgkmcnt(0)).
+__device__ inline void stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Issue the direct loads of one k-stage (A then B, 16 KB each) into LDS
+// buffer `buf`: each wave copies 1 KB contiguous per instruction.
+__device__ inline void load_stage(const int8_t *A, const int8_t *B, int8_t *buf, int tid, int wave) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        __builtin_amdgcn_global_load_lds(A + q * 8192 + tid * 16, (lds_void *)(buf + q * 8192 + wave * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(B + q * 8192 + tid * 16,
+                                         (lds_void *)(buf + kStageBytes + q * 8192 + wave * 1024), 16, 0, 0);
+    }
+}
+
+// Operand fragments of a wave (128 rows of A, 64 rows of B) for one stage.
+__device__ inline void read_a(const int8_t *buf, int wr, int lane, int i0, v4i (&a)[8]) {
+#pragma unroll
+    for (int i = i0; i < i0 + 4; ++i) a[i] = *reinterpret_cast<const v4i *>(buf + (wr * 8 + i) * kFragBytes + lane * 16);
+}
+__device__ inline void read_b(const int8_t *buf, int wc, int lane, v4i (&b)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const v4i *>(buf + kStageBytes + (wc * 4 + j) * kFragBytes + lane * 16);
+}
+
+// 16 MFMAs: accumulator rows i0..i0+3 against all 4 B fragments.
+__device__ inline void mfma_half(v4i (&acc)[8][4], const v4i (&a)[8], const v4i (&b)[4], int i0) {
+#pragma unroll
+    for (int i = i0; i < i0 + 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
 }
 
 __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
-    __shared__ __attribute__((aligned(16))) int8_t lds[kLdsBytes];
+    __shared__ __attribute__((aligned(1024))) int8_t lds[kLdsBytes];
 
-    const int tiles = g.mt * g.nt;
-    const int total = tiles * g.batch;
-    const int b = xcd_remap((int)blockIdx.x, total);
-    const int p = b / tiles;
-    const int t = b - p * tiles;
-    const int group = t / (kGroupRows * g.nt);
-    const int first = group * kGroupRows;
-    const int gsize = min(g.mt - first, kGroupRows);
-    const int within = t - group * kGroupRows * g.nt;
-    const int ti = first + within % gsize;
-    const int tj = within / gsize;
+    const TileCoord tc = tile_of((int)blockIdx.x, g.mt, g.nt, g.chunk);
+    if (!tc.valid) return;  // whole workgroup: no barrier is pending
+    const int p = tc.p, ti = tc.ti, tj = tc.tj;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wr = wave >> 1, wc = wave & 1;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
+    const int wr = wave >> 2, wc = wave & 3;                     // 2 x 4 waves of 128 x 64
+    const int KB = g.kblocks;
 
-    const int8_t *A = g.a + (size_t)p * g.a_pstride + (size_t)ti * g.kblocks * kStageBytes + tid * 16;
-    const int8_t *B = g.b + (size_t)p * g.b_pstride + (size_t)tj * g.kblocks * kStageBytes + tid * 16;
+    const int8_t *A = g.a + (size_t)p * g.a_pstride + (size_t)ti * KB * kStageBytes;
+    const int8_t *B = g.b + (size_t)p * g.b_pstride + (size_t)tj * KB * kStageBytes;
 
-    v16i acc[4][4];
+    v4i acc[8][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = v16i{};
+        for (int j = 0; j < 4; ++j) acc[i][j] = v4i{};
 
-    v4i sa[4], sb[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        sa[q] = *reinterpret_cast<const v4i *>(A + q * 4096);
-        sb[q] = *reinterpret_cast<const v4i *>(B + q * 4096);
+    // prologue: fill the ring, then wait for stage 0
+    const int pre = KB < kStages ? KB : kStages;
+    for (int s = 0; s < pre; ++s)
+        load_stage(A + (size_t)s * kStageBytes, B + (size_t)s * kStageBytes, lds + s * kStageBuf, tid, wave);
+    switch (pre) {
+    case 1: wait_vm<0>(); break;
+    case 2: wait_vm<kLoadsPerStage>(); break;
+    case 3: wait_vm<2 * kLoadsPerStage>(); break;
+    default: wait_vm<3 * kLoadsPerStage>(); break;
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        *reinterpret_cast<v4i *>(lds + q * 4096 + tid * 16) = sa[q];
-        *reinterpret_cast<v4i *>(lds + kStageBytes + q * 4096 + tid * 16) = sb[q];
-    }
-    __syncthreads();
+    stage_barrier();
 
-    for (int kb = 0; kb < g.kblocks; ++kb) {
-        const int8_t *cur = lds + (kb & 1) * (2 * kStageBytes);
-        const bool more = kb + 1 < g.kblocks;
-        if (more) {
-            const size_t off = (size_t)(kb + 1) * kStageBytes;
+    v4i fa[8], fb[4], nb[4];
+    read_a(lds, wr, lane, 0, fa);
+    read_b(lds, wc, lane, fb);
+
+    // One k-stage: rows 4..7 of A are read while the MFMAs of rows 0..3 run;
+    // the barrier that recycles this stage's buffer sits between the two MFMA
+    // halves; the next stage's rows 0..3 of A and its B are read while the
+    // MFMAs of rows 4..7 run.  The last stage is peeled off so that every
+    // iteration has the same LDS-counter state (no conservative waits).
+    for (int kb = 0; kb + 1 < KB; ++kb) {
+        const int8_t *buf = lds + (kb % kStages) * kStageBuf;
+        wait_lds();
+        read_a(buf, wr, lane, 4, fa);
+        sched_fence();
+        mfma_half(acc, fa, fb, 0);
+        sched_fence();
+        const bool load = kb + kStages < KB;
+        if (load) wait_vm<kLoadsPerStage * (kStages - 2)>();  // stage kb+1 landed
+        else wait_vm<0>();
+        stage_barrier();  // every wave is done reading stage kb: recycle its buffer
+        if (load)
+            load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
+                       lds + (kb % kStages) * kStageBuf, tid, wave);
+        const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
+        read_a(nbuf, wr, lane, 0, fa);
+        read_b(nbuf, wc, lane, nb);
+        sched_fence();
+        mfma_half(acc, fa, fb, 4);
+        sched_fence();
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                sa[q] = *reinterpret_cast<const v4i *>(A + off + q * 4096);
-                sb[q] = *reinterpret_cast<const v4i *>(B + off + q * 4096);
-            }
-        }
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            v4i fa[4], fb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                fa[i] = *reinterpret_cast<const v4i *>(cur + (ks * 8 + wr * 4 + i) * kFragBytes + lane * 16);
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                fb[j] = *reinterpret_cast<const v4i *>(cur + kStageBytes + (ks * 8 + wc * 4 + j) * kFragBytes + lane * 16);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);
-        }
-        if (more) {
-            int8_t *nxt = lds + ((kb + 1) & 1) * (2 * kStageBytes);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<v4i *>(nxt + q * 4096 + tid * 16) = sa[q];
-                *reinterpret_cast<v4i *>(nxt + kStageBytes + q * 4096 + tid * 16) = sb[q];
-            }
-        }
-        __syncthreads();
+        for (int j = 0; j < 4; ++j) fb[j] = nb[j];
     }
+    wait_lds();
+    read_a(lds + ((KB - 1) % kStages) * kStageBuf, wr, lane, 4, fa);
+    mfma_half(acc, fa, fb, 0);
+    mfma_half(acc, fa, fb, 4);
 
     // ---- epilogue: C mod m -> int8, staged through LDS, coalesced store ----
+    // v_mfma_i32_16x16x64_i8 leaves column (lane % 16), rows 4 (lane / 16) + e
+    // of its 16 x 16 block in element e: 4 consecutive rows make one dword.
+    stage_barrier();  // every wave is done with the ring; no loads are in flight
     const int mi = p >> g.mod_shift;
     const double inv = g.inv[mi];
     const uint32_t negm = (uint32_t)(-g.mod[mi]) & 0xFFFFFFu;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 8; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int col = wc * 128 + j * 32 + (lane & 31);
+            uint32_t by[4];
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                uint32_t by[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int v = acc[i][j][4 * g4 + r];
-                    const double q = fma((double)v, inv, kMagic);
-                    by[r] = mad24(lo32(q), negm, (uint32_t)v);
-                }
-                const int row = wr * 128 + i * 32 + 8 * g4 + 4 * (lane >> 5);
-                *reinterpret_cast<uint32_t *>(lds + col * kEpiStride + row) = pack4(by[0], by[1], by[2], by[3]);
+            for (int e = 0; e < 4; ++e) {
+                const int v = acc[i][j][e];
+                const double q = fma((double)v, inv, kMagic);   // 1.5 2^52 + rint(v / m)
+                by[e] = mad24(lo32(q), negm, (uint32_t)v);     // v - q m (low byte)
             }
+            const int col = wc * 64 + j * 16 + (lane & 15);
+            const int row = wr * 128 + i * 16 + 4 * (lane >> 4);
+            *reinterpret_cast<uint32_t *>(lds + col * kEpiStride + row) = pack4(by[0], by[1], by[2], by[3]);
         }
     }
     __syncthreads();
     int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256) * g.ldc + ti * 256;
     const int ch = tid & 15;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const int c = (tid >> 4) + 16 * q;
+    for (int q = 0; q < 8; ++q) {
+        const int c = (tid >> 4) + 32 * q;
         *reinterpret_cast<uint4 *>(C + (size_t)c * g.ldc + ch * 16) =
             *reinterpret_cast<const uint4 *>(lds + c * kEpiStride + ch * 16);
     }
@@ -172,9 +243,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmArgs &ga, hipStream_t st) {
-    const long total = (long)ga.mt * ga.nt * ga.batch;
-    if (total <= 0 || ga.kblocks <= 0) return hipSuccess;
+hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
+    static_assert(kThreads * 16 * kLoadsPerStage == 2 * kStageBytes, "stage copy covers A and B");
+    GemmArgs ga = ga_in;
+    const long tiles = (long)ga.mt * ga.nt;
+    if (tiles <= 0 || ga.batch <= 0 || ga.kblocks <= 0) return hipSuccess;
+    ga.chunk = (int)((tiles + 7) / 8);
+    const long total = 8L * ga.chunk * ga.batch;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
     gemm_i8_kernel<<<(unsigned)total, kThreads, 0, st>>>(ga);
     return hipGetLastError();

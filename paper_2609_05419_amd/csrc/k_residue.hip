@@ -77,14 +77,14 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
                                                       ResidueParams rp, int8_t *planes) {
     const int lane = threadIdx.x & 63;
     const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);   // one wave = one fragment
-    const int frows = rows_pad >> 5;                          // fragments along rows
-    const int fks = kblocks * 2;                              // fragments along k
+    const int frows = rows_pad / kFragRows;                   // fragments along rows
+    const int fks = kblocks;                                  // fragments along k
     int fr, fk;
     if (wave >= frows * fks) return;
     if (MODE == 1) { fk = wave % fks; fr = wave / fks; }      // B: walk k fastest (contiguous)
     else { fr = wave % frows; fk = wave / frows; }            // A: walk rows fastest
-    const int r = fr * 32 + (lane & 31);
-    const int kk0 = fk * 32 + (lane >> 5) * 16;
+    const int r = fr * kFragRows + (lane & 15);
+    const int kk0 = fk * kStageK + (lane >> 4) * 16;
 
     // ---- load and quantize (step 3) -------------------------------------
     double x1r[kPerThread], x0r[kPerThread], x1i[kPerThread], x0i[kPerThread];
@@ -162,7 +162,7 @@ hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const i
                            int khalf, const PlaneGeom &g, const ResidueParams &rp, int8_t *planes,
                            hipStream_t st) {
     const int kreal = khalf > 0 ? g.kreal : 0;
-    const long waves = (long)(g.rows_pad / 32) * (long)(g.kblocks * 2);
+    const long waves = (long)(g.rows_pad / kFragRows) * (long)g.kblocks;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
     const bool split3 = shift > 62;
 #define O2M_RES(M, T, S3, SC)                                                                    \

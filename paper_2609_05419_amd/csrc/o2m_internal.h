@@ -19,28 +19,29 @@ constexpr int kStatusOverflow = 1;  // device status bit: gauss-mode bound viola
 // Every operand plane is R_pad x K_pad int8 values, "K-major": the row index
 // is a row of A (or a column of B) and k runs inside.  It is stored in the
 // order the int8 GEMM consumes it, so that one wave reads one MFMA fragment as
-// a single contiguous 1 KB and one thread block reads one pipeline stage as a
-// single contiguous 32 KB:
+// a single contiguous 1 KB and one thread block copies one pipeline stage as a
+// single contiguous 16 KB per operand:
 //
 //   block of 256 rows x 64 k       = one GEMM stage for one operand (16 KB)
-//   fragment of 32 rows x 32 k     = one v_mfma_i32_32x32x32_i8 operand (1 KB)
-//   lane chunk of 1 row x 16 k     = 16 bytes held by one lane
+//   fragment of 16 rows x 64 k     = one v_mfma_i32_16x16x64_i8 operand (1 KB)
+//   lane chunk of 1 row x 16 k     = the 16 bytes one lane holds
 //
-// offset(r, kk) = ((rb*KB + kb)*16 + ks*8 + rg)*1024 + lane*16 + (kk & 15)
-// with rb = r/256, rg = (r%256)/32, kb = kk/64, ks = (kk%64)/32,
-// lane = (r%32) + 32*((kk%32)/16), KB = K_pad/64.
+// offset(r, kk) = ((rb*KB + kb)*16 + rg)*1024 + lane*16 + (kk & 15)
+// with rb = r/256, rg = (r%256)/16, kb = kk/64,
+// lane = (r%16) + 16*((kk%64)/16), KB = K_pad/64.
 // ---------------------------------------------------------------------------
 constexpr int kRowBlock = 256;
 constexpr int kStageK = 64;
+constexpr int kFragRows = 16;
 constexpr int kFragBytes = 1024;
 constexpr int kStageBytes = kRowBlock * kStageK;  // 16 KB per operand per stage
 
 __host__ __device__ inline size_t plane_offset(int r, int kk, int kblocks) {
     const int rb = r >> 8, rr = r & 255;
     const int kb = kk >> 6, kr = kk & 63;
-    const int rg = rr >> 5, ks = kr >> 5;
-    const int lane = (rr & 31) + (((kr & 31) >> 4) << 5);
-    return ((size_t)(rb * kblocks + kb) * 16 + ks * 8 + rg) * kFragBytes + lane * 16 + (kr & 15);
+    const int rg = rr >> 4;
+    const int lane = (rr & 15) + ((kr >> 4) << 4);
+    return ((size_t)(rb * kblocks + kb) * 16 + rg) * kFragBytes + lane * 16 + (kr & 15);
 }
 
 inline int round_up(int x, int q) { return (x + q - 1) / q * q; }
@@ -136,6 +137,7 @@ struct GemmArgs {
     int batch;
     int mod_shift;
     int ldc;
+    int chunk;                               // tiles per XCD per product (set by the launcher)
     int mod[kMaxModuli];
     double inv[kMaxModuli];
 };
