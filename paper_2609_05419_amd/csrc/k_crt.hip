@@ -12,102 +12,17 @@
 // q = rint(X / M) is estimated from a fp64 Horner sum; the scaling budget keeps
 // |c| / M <= 1/2 - 2^-32, far from the rounding boundary, so q is exact.  The
 // lifted value c = X - q M (step 6) is then exact as limbs c_t = S_t - q M_t,
-// assembled into a 192-bit two's complement integer and rounded to the nearest
-// double, ties to even, and scaled by 2^(E_i + F_j - pA - pB) (step 7).
+// rounded to the nearest double, ties to even (a correctly rounded three-term
+// sum for T <= 3 limbs, a 192-bit integer for T = 4: crt_round.h), and scaled
+// by 2^(E_i + F_j - pA - pB) (step 7).
 //
 // Bound: HBM.  Algorithmic bytes per output entry: 2N residues read + 16
 // written (complex fp64; 8 for complex fp32).
 #include "o2m_internal.h"
+#include "crt_round.h"
 
 namespace o2m {
 namespace {
-
-constexpr double kTwo40 = 1099511627776.0;
-
-struct U192 {
-    uint64_t w0, w1, w2;
-};
-
-// a += x * 2^s (two's complement, modulo 2^192); s is a compile-time multiple of 40
-__device__ inline void add_shifted(U192 &a, int64_t x, int s) {
-    const uint64_t ux = (uint64_t)x;
-    const uint64_t ext = (uint64_t)(x >> 63);
-    uint64_t y0, y1, y2;
-    if (s == 0) {
-        y0 = ux; y1 = ext; y2 = ext;
-    } else if (s < 64) {
-        y0 = ux << s; y1 = (ux >> (64 - s)) | (ext << s); y2 = ext;
-    } else if (s < 128) {
-        const int t = s - 64;
-        y0 = 0; y1 = ux << t; y2 = (ux >> (64 - t)) | (ext << t);
-    } else {
-        y0 = 0; y1 = 0; y2 = ux << (s - 128);
-    }
-    const uint64_t r0 = a.w0 + y0;
-    const uint64_t c0 = r0 < y0;
-    uint64_t r1 = a.w1 + y1;
-    uint64_t c1 = r1 < y1;
-    r1 += c0;
-    c1 += r1 < c0;
-    a.w0 = r0;
-    a.w1 = r1;
-    a.w2 = a.w2 + y2 + c1;
-}
-
-// Round the 192-bit signed integer v to the nearest double (ties to even) and
-// multiply by 2^sc, rounding once.
-__device__ inline double round_scaled(U192 v, int sc) {
-    const bool neg = (int64_t)v.w2 < 0;
-    if (neg) {
-        v.w0 = ~v.w0; v.w1 = ~v.w1; v.w2 = ~v.w2;
-        v.w0 += 1;
-        const uint64_t c0 = v.w0 == 0;
-        v.w1 += c0;
-        v.w2 += (c0 && v.w1 == 0);
-    }
-    int lz;
-    if (v.w2) lz = __clzll(v.w2);
-    else if (v.w1) lz = 64 + __clzll(v.w1);
-    else if (v.w0) lz = 128 + __clzll(v.w0);
-    else return 0.0;
-    uint64_t h, rest_nonzero;
-    if (lz >= 128) {
-        h = v.w0 << (lz - 128);
-        rest_nonzero = 0;
-    } else if (lz >= 64) {
-        const int s = lz - 64;
-        h = s ? (v.w1 << s) | (v.w0 >> (64 - s)) : v.w1;
-        rest_nonzero = s ? (v.w0 << s) : v.w0;
-    } else {
-        const int s = lz;
-        h = s ? (v.w2 << s) | (v.w1 >> (64 - s)) : v.w2;
-        const uint64_t n1 = s ? (v.w1 << s) | (v.w0 >> (64 - s)) : v.w1;
-        const uint64_t n0 = s ? (v.w0 << s) : v.w0;
-        rest_nonzero = n1 | n0;
-    }
-    uint64_t mant = h >> 11;
-    const uint64_t rb = h & 0x7FF;
-    if (rb > 0x400 || (rb == 0x400 && (rest_nonzero != 0 || (mant & 1)))) mant += 1;
-    const int top = 191 - lz;
-    const double r = ldexp((double)mant, top - 52 + sc);
-    return neg ? -r : r;
-}
-
-// Step 5-6: from the limb sums, the exact lifted integer c as 192 bits.
-template <int T>
-__device__ inline U192 lift(const double (&S)[T], const CrtParams &cp) {
-    double X = S[T - 1];
-#pragma unroll
-    for (int t = T - 2; t >= 0; --t) X = fma(X, kTwo40, S[t]);
-    const double q = rint(X * cp.inv_m);
-    U192 v = {0, 0, 0};
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-        const double ct = fma(-q, cp.mlimb[t], S[t]);
-        add_shifted(v, (int64_t)ct, 40 * t);
-    }
-    return v;
-}
 
 __device__ inline int sext8(uint32_t w, int e) { return (int)(int8_t)(w >> (8 * e)); }
 
@@ -124,23 +39,24 @@ template <> struct Out<kF32> {
 };
 
 // MODE 0: ZGEMM / CGEMM output.  MODE 3: exact Gaussian integers (int64).
-// MODE 4: residue hook (per-modulus 2M post output).
-template <int T, int MODE, ElemType OT>
+// MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R
+// consecutive rows of one column (R = 4: one dword per plane; R = 8: two).
+template <int T, int MODE, ElemType OT, int R>
 __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
-    const int mblocks = (a.m + 1023) / 1024;
+    const int rows_per_block = 256 * R;
+    const int mblocks = (a.m + rows_per_block - 1) / rows_per_block;
     const int j = blockIdx.x / mblocks;
-    const int i0 = ((blockIdx.x % mblocks) * 256 + threadIdx.x) * 4;
+    const int i0 = ((blockIdx.x % mblocks) * 256 + threadIdx.x) * R;
     if (i0 >= a.m) return;
     const int8_t *base = a.res + (size_t)j * a.ldr + i0;
 
     if (MODE == 4) {
         for (int l = 0; l < a.rp.n; ++l) {
-            const uint32_t wp = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l) * a.plane_bytes);
-            const uint32_t wm = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
             const int m = a.rp.mod[l], s = a.rp.root[l], half = (m + 1) / 2;
             int8_t *out = reinterpret_cast<int8_t *>(a.c);
-            for (int e = 0; e < 4 && i0 + e < a.m; ++e) {
-                const int rp = sext8(wp, e), rm = sext8(wm, e);
+            for (int e = 0; e < R && i0 + e < a.m; ++e) {
+                const int rp = base[(size_t)(2 * l) * a.plane_bytes + e];
+                const int rm = base[(size_t)(2 * l + 1) * a.plane_bytes + e];
                 int re = ((half * (rm + rp)) % m + m) % m;
                 int im = ((s * ((half * (rm - rp)) % m)) % m + m) % m;
                 if (re > (m - 1) / 2) re -= m;
@@ -153,18 +69,26 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
         return;
     }
 
-    double sre[4][T], sim[4][T];
+    double sre[R][T], sim[R][T];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int e = 0; e < R; ++e)
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
     for (int l = 0; l < cp.n; ++l) {
-        const uint32_t wp = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l) * a.plane_bytes);
-        const uint32_t wm = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
+        uint32_t wp[R / 4], wm[R / 4];
+        if (R == 8) {
+            const uint2 p2 = *reinterpret_cast<const uint2 *>(base + (size_t)(2 * l) * a.plane_bytes);
+            const uint2 m2 = *reinterpret_cast<const uint2 *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
+            wp[0] = p2.x; wp[R / 4 - 1] = p2.y;
+            wm[0] = m2.x; wm[R / 4 - 1] = m2.y;
+        } else {
+            wp[0] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l) * a.plane_bytes);
+            wm[0] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
+        }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int rp = sext8(wp, e), rm = sext8(wm, e);
+        for (int e = 0; e < R; ++e) {
+            const int rp = sext8(wp[e >> 2], e & 3), rm = sext8(wm[e >> 2], e & 3);
             const double u = (double)(rm + rp), v = (double)(rm - rp);
 #pragma unroll
             for (int t = 0; t < T; ++t) {
@@ -175,12 +99,12 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     }
 
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < R; ++e) {
         const int i = i0 + e;
         if (i >= a.m) break;
-        const U192 vre = lift<T>(sre[e], cp);
-        const U192 vim = lift<T>(sim[e], cp);
         if (MODE == 3) {
+            const U192 vre = lift_exact<T>(sre[e], cp.mlimb, cp.inv_m);
+            const U192 vim = lift_exact<T>(sim[e], cp.mlimb, cp.inv_m);
             // exact Gaussian integers: M < 2^63, fix the lift into [-h, h]
             int64_t re = (int64_t)vre.w0, im = (int64_t)vim.w0;
             const int64_t M = (int64_t)cp.m_lo, h = (int64_t)cp.h_lo;
@@ -203,8 +127,8 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
                 im = re;
             } else {
                 const int sc = ei + fj + a.scale_bias;
-                re = round_scaled(vre, sc);
-                im = round_scaled(vim, sc);
+                re = lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
+                im = lift_round<T>(sim[e], cp.mlimb, cp.inv_m, sc);
             }
             Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, re, im);
         }
@@ -266,11 +190,11 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
         const bool bad = ei == INT32_MIN || ej == INT32_MIN;
         const int sc = ei + ej + a.scale_bias;
         if (REAL_ONLY) {
-            const double re = bad ? __builtin_nan("") : round_scaled(lift<T>(sre[e], cp), sc);
+            const double re = bad ? __builtin_nan("") : lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
             reinterpret_cast<double *>(a.c)[(size_t)i + (size_t)j * a.ldc] = re;
         } else {
-            const double re = bad ? __builtin_nan("") : round_scaled(lift<T>(sre[e], cp), sc);
-            const double im = bad ? __builtin_nan("") : round_scaled(lift<T>(sim[e], cp), sc);
+            const double re = bad ? __builtin_nan("") : lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
+            const double im = bad ? __builtin_nan("") : lift_round<T>(sim[e], cp.mlimb, cp.inv_m, sc);
             reinterpret_cast<double2 *>(a.c)[(size_t)i + (size_t)j * a.ldc] = make_double2(re, im);
         }
     }
@@ -285,12 +209,16 @@ hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &c
         else crt_sym_kernel<T, true><<<blocks, 256, 0, st>>>(ca, cp);
         return hipGetLastError();
     }
-    const long blocks = (long)((ca.m + 1023) / 1024) * ca.n;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    if (mode == 0 && ot == kF64) crt_kernel<T, 0, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 0 && ot == kF32) crt_kernel<T, 0, kF32><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 3) crt_kernel<T, 3, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 4) crt_kernel<T, 4, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    // 8 rows per thread when the residue rows are 8-byte aligned (ldr is a
+    // multiple of 256) and the limb count leaves room in registers
+    constexpr int R = 4;
+    const long blocks = (long)((ca.m + 256 * R - 1) / (256 * R)) * ca.n;
+    const long blocks4 = (long)((ca.m + 1023) / 1024) * ca.n;
+    if (blocks > 0x7FFFFFFF || blocks4 > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (mode == 0 && ot == kF64) crt_kernel<T, 0, kF64, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    else if (mode == 0 && ot == kF32) crt_kernel<T, 0, kF32, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    else if (mode == 3) crt_kernel<T, 3, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
+    else if (mode == 4) crt_kernel<T, 4, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
