@@ -86,7 +86,21 @@ def main() -> int:
     ap.add_argument("--phi", type=float, default=0.5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-native", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only copy 1 GiB device-to-device twice (reference kernel for the "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE scale) and exit")
     args = ap.parse_args()
+
+    if args.calibrate_copy:
+        import torch
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: copied {n} bytes twice")
+        return 0
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -191,7 +205,7 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline on a sample")
-        cpu = cpu_baseline(a, b, N, rows=min(m, 1024), cols=min(n, 1536))
+        cpu = cpu_baseline(a, b, N, rows=min(m, 1536), cols=min(n, 2048))
 
     line = {
         "metric": "effective ZGEMM TFLOP/s (8mnk/t) at m=n=k=8192 + int8 MFMA util %",

@@ -175,9 +175,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     read_b(lds, wc, lane, fb);
 
     // One k-stage: rows 4..7 of A are read while the MFMAs of rows 0..3 run;
-    // the barrier that recycles this stage's buffer sits between the two MFMA
+    // the barrier that frees this stage's buffer sits between the two MFMA
     // halves; the next stage's rows 0..3 of A and its B are read while the
-    // MFMAs of rows 4..7 run.  The last stage is peeled off so that every
+    // MFMAs of rows 4..7 run, and the freed buffer is refilled after them.  The last stage is peeled off so that every
     // iteration has the same LDS-counter state (no conservative waits).
     for (int kb = 0; kb + 1 < KB; ++kb) {
         const int8_t *buf = lds + (kb % kStages) * kStageBuf;
@@ -186,19 +186,23 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
         sched_fence();
         mfma_half(acc, fa, fb, 0);
         sched_fence();
-        const bool load = kb + kStages < KB;
-        if (load) wait_vm<kLoadsPerStage * (kStages - 2)>();  // stage kb+1 landed
+        // stage kb+1 must have landed; stages kb+2, kb+3 may stay in flight
+        const int younger = min(KB - 1, kb + kStages - 1) - (kb + 1);
+        if (younger >= 2) wait_vm<2 * kLoadsPerStage>();
+        else if (younger == 1) wait_vm<kLoadsPerStage>();
         else wait_vm<0>();
-        stage_barrier();  // every wave is done reading stage kb: recycle its buffer
-        if (load)
-            load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
-                       lds + (kb % kStages) * kStageBuf, tid, wave);
+        stage_barrier();  // every wave is done reading stage kb: its buffer is free
         const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
         read_a(nbuf, wr, lane, 0, fa);
         read_b(nbuf, wc, lane, nb);
         sched_fence();
         mfma_half(acc, fa, fb, 4);
         sched_fence();
+        // refill the freed buffer after the MFMAs, so that the fragment reads
+        // above are not queued behind the stage copy
+        if (kb + kStages < KB)
+            load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
+                       lds + (kb % kStages) * kStageBuf, tid, wave);
 #pragma unroll
         for (int j = 0; j < 4; ++j) fb[j] = nb[j];
     }
