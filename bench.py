@@ -77,6 +77,7 @@ def cpu_baseline(a, b, n_moduli, rows, cols):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--op", choices=("zgemm", "cgemm", "zherk", "dsyrk"), default="zgemm")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--m", type=int, default=8192)
@@ -112,21 +113,74 @@ def main() -> int:
     import paper_2609_05419_amd as o2m
     import workloads
 
+    op = args.op
     m, n, k, N = args.m, args.n, args.k, args.n_moduli
+    if op in ("zherk", "dsyrk"):
+        n = m
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    sa, sb = workloads.config_seeds(3)
-    log(f"bench: generating inputs {m}x{k} and {k}x{n} (phi={args.phi})")
-    a = workloads.complex_matrix(m, k, sa, dist="phi", phi=args.phi)
-    b = workloads.complex_matrix(k, n, sb, dist="phi", phi=args.phi)
-    A = torch.from_numpy(np.ascontiguousarray(a.T)).to(dev).t()
-    B = torch.from_numpy(np.ascontiguousarray(b.T)).to(dev).t()
-    C = torch.empty((n, m), dtype=torch.complex128, device=dev).t()
     stream = torch.cuda.current_stream()
+
+    def to_dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x.T)).to(dev).t()
+
+    cfg = {"zgemm": 3, "cgemm": 4, "zherk": 5, "dsyrk": 5}[op]
+    sa, sb = workloads.config_seeds(cfg)
+    log(f"bench: {op} m={m} n={n} k={k} N={N}: generating inputs")
+    if op == "zgemm":
+        a = workloads.complex_matrix(m, k, sa, dist="phi", phi=args.phi)
+        b = workloads.complex_matrix(k, n, sb, dist="phi", phi=args.phi)
+        A, B = to_dev(a), to_dev(b)
+        C = torch.empty((n, m), dtype=torch.complex128, device=dev).t()
+        call = lambda: o2m.zgemm_2m(A, B, n_moduli=N, out=C)
+        flops, int8_ops = 8.0 * m * n * k, 4.0 * N * m * n * k
+        metric = ("effective ZGEMM TFLOP/s (8mnk/t) at m=n=k=8192 + int8 MFMA util %"
+                  if (m, n, k) == (8192, 8192, 8192) else "effective ZGEMM TFLOP/s (8mnk/t)")
+        desc = (f"zgemm_2m {m}x{n}x{k} complex128, parts U(-0.5,0.5)*exp({args.phi}*N(0,1)), "
+                f"{N} 2M moduli, int8 MFMA")
+        pre_bytes = (16.0 + 2 * N) * (m * k + k * n)
+        scale_bytes = 16.0 * (m * k + k * n)
+        post_bytes = (2.0 * N + 16.0) * m * n
+    elif op == "cgemm":
+        a = workloads.complex_matrix(m, k, sa, dist="uniform", dtype=np.complex64)
+        b = workloads.complex_matrix(k, n, sb, dist="uniform", dtype=np.complex64)
+        A, B = to_dev(a), to_dev(b)
+        C = torch.empty((n, m), dtype=torch.complex64, device=dev).t()
+        call = lambda: o2m.cgemm_2m(A, B, n_moduli=N, out=C)
+        flops, int8_ops = 8.0 * m * n * k, 4.0 * N * m * n * k
+        metric = "effective CGEMM TFLOP/s (8mnk/t)"
+        desc = f"cgemm_2m {m}x{n}x{k} complex64, parts U(-1,1), {N} 2M moduli, int8 MFMA"
+        pre_bytes = (8.0 + 2 * N) * (m * k + k * n)
+        scale_bytes = 8.0 * (m * k + k * n)
+        post_bytes = (2.0 * N + 8.0) * m * n
+    elif op == "zherk":
+        a = workloads.complex_matrix(n, k, sa)
+        A = to_dev(a)
+        C = o2m.colmajor(torch.zeros((n, n), dtype=torch.complex128, device=dev))
+        call = lambda: o2m.zherk_2m(A, n_moduli=N, out=C)
+        flops, int8_ops = 4.0 * n * n * k, 2.0 * N * n * n * k
+        metric = "effective ZHERK TFLOP/s (4n^2k/t)"
+        desc = f"zherk_2m n={n} k={k} complex128 N(0,1), {N} 2M moduli, lower triangle"
+        pre_bytes = (16.0 + 2 * N) * n * k
+        scale_bytes = 16.0 * n * k
+        post_bytes = (N + 8.0) * n * n           # both triangles of C+ read, lower C written
+    else:  # dsyrk
+        a = workloads.real_matrix(n, k, sa)
+        A = to_dev(a)
+        C = o2m.colmajor(torch.zeros((n, n), dtype=torch.float64, device=dev))
+        call = lambda: o2m.dsyrk_2m(A, n_moduli=N, out=C)
+        flops, int8_ops = 1.0 * n * n * k, 2.0 * N * n * n * ((k + 1) // 2)
+        metric = "effective DSYRK TFLOP/s (n^2k/t)"
+        desc = f"dsyrk_2m n={n} k={k} float64 N(0,1), {N} 2M moduli, lower triangle"
+        pre_bytes = (8.0 + N) * n * k
+        scale_bytes = 8.0 * n * k
+        post_bytes = (N + 4.0) * n * n
+    x = None
+    a_host, b_host = a, (b if op in ("zgemm", "cgemm") else None)
 
     log(f"bench: warmup {args.warmup}")
     for _ in range(args.warmup):
-        o2m.zgemm_2m(A, B, n_moduli=N, out=C)
+        call()
     torch.cuda.synchronize()
 
     log(f"bench: timing {args.steps} steps")
@@ -136,7 +190,7 @@ def main() -> int:
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
-        o2m.zgemm_2m(A, B, n_moduli=N, out=C)
+        call()
     end.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
@@ -144,19 +198,13 @@ def main() -> int:
     o2m.phase_timing(False)
     log(f"bench: {ms:.3f} ms/step, phases {phases}")
 
-    flops = 8.0 * m * n * k
     value = flops / (ms * 1e-3) / 1e12
-    int8_ops = 4.0 * N * m * n * k            # 2N int8 GEMMs of 2mnk ops
     gemm_ms = phases.get("int8_gemm", float("nan"))
     achieved = int8_ops / (gemm_ms * 1e-3) / 1e12
-    workload_key = f"zgemm m{m} n{n} k{k} N{N} phi{args.phi}"
+    workload_key = f"{op} m{m} n{n} k{k} N{N} phi{args.phi}"
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_INT8_TOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
                 "traffic": load_traffic(workload_key)}
-    # the bandwidth-bound phases, against HBM
-    pre_bytes = (16.0 + 2 * N) * (m * k + k * n)          # read complex, write 2N int8 planes
-    scale_bytes = 16.0 * (m * k + k * n)
-    post_bytes = (2.0 * N + 16.0) * m * n
     hbm = {
         "scale_GBs": round(scale_bytes / (phases["scale"] * 1e-3) / 1e9, 1),
         "residues_GBs": round(pre_bytes / (phases["residues"] * 1e-3) / 1e9, 1),
@@ -164,25 +212,29 @@ def main() -> int:
         "peak_GBs": PEAK_HBM_GBS,
     }
 
-    # sampled accuracy against the double-double reference
+    # sampled accuracy against the double-double reference (GEMMs)
     accuracy = None
-    try:
-        import oracle
-        rng = np.random.default_rng(8)
-        ent = [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 64), rng.integers(0, n, 64))]
-        Ch = C.cpu().numpy()
-        got = np.array([Ch[i, j] for i, j in ent])
-        hi, lo = oracle.dd_gemm(a, b, entries=ent)
-        absab = np.array([np.sum(np.abs(a[i, :]) * np.abs(b[:, j])) for i, j in ent])
-        err = oracle.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -53)
-        exact = oracle.oq_zgemm(a, b, N, entries=ent)
-        accuracy = {"sampled_entries": len(ent), "maxrel": err["maxrel"], "tol_ratio": err["ratio"],
-                    "bit_exact_vs_oracle": bool(np.array_equal(got.view(np.uint64), exact.view(np.uint64)))}
-    except Exception as e:  # accuracy is a report, not the metric
-        log(f"bench: accuracy check skipped: {e}")
+    if op in ("zgemm", "cgemm"):
+        try:
+            import oracle
+            rng = np.random.default_rng(8)
+            ent = [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 64), rng.integers(0, n, 64))]
+            Ch = C.cpu().numpy()
+            got = np.array([Ch[i, j] for i, j in ent])
+            a64, b64 = a_host.astype(np.complex128), b_host.astype(np.complex128)
+            hi, lo = oracle.dd_gemm(a64, b64, entries=ent)
+            absab = np.array([np.sum(np.abs(a64[i, :]) * np.abs(b64[:, j])) for i, j in ent])
+            u = 2.0 ** -53 if op == "zgemm" else 2.0 ** -24
+            err = oracle.error_vs_reference(got.astype(np.complex128), absab, hi, lo, k, u)
+            exact = (oracle.oq_zgemm(a_host, b_host, N, entries=ent) if op == "zgemm"
+                     else oracle.oq_cgemm(a_host, b_host, N, entries=ent))
+            accuracy = {"sampled_entries": len(ent), "maxrel": err["maxrel"], "tol_ratio": err["ratio"],
+                        "bit_exact_vs_oracle": bool(np.array_equal(got, exact))}
+        except Exception as e:  # accuracy is a report, not the metric
+            log(f"bench: accuracy check skipped: {e}")
 
     native = None
-    if not args.no_native:
+    if not args.no_native and op in ("zgemm", "cgemm"):
         try:
             for _ in range(2):
                 Cn = torch.matmul(A, B)
@@ -196,19 +248,19 @@ def main() -> int:
             e2.record(stream)
             torch.cuda.synchronize()
             nms = s2.elapsed_time(e2) / reps
-            native = {"op": "torch.matmul complex128", "ms": round(nms, 3),
+            native = {"op": f"torch.matmul {A.dtype}".replace("torch.", ""), "ms": round(nms, 3),
                       "tflops": round(flops / (nms * 1e-3) / 1e12, 2)}
             del Cn
         except Exception as e:
             log(f"bench: native comparison skipped: {e}")
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and op == "zgemm":
         log("bench: CPU oracle baseline on a sample")
-        cpu = cpu_baseline(a, b, N, rows=min(m, 1536), cols=min(n, 2048))
+        cpu = cpu_baseline(a_host, b_host, N, rows=min(m, 1536), cols=min(n, 2048))
 
     line = {
-        "metric": "effective ZGEMM TFLOP/s (8mnk/t) at m=n=k=8192 + int8 MFMA util %",
+        "metric": metric,
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -220,9 +272,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": f"zgemm_2m {m}x{n}x{k} complex128, parts U(-0.5,0.5)*exp({args.phi}*N(0,1)), "
-                               f"{N} 2M moduli, int8 MFMA", "m": m, "n": n, "k": k, "n_moduli": N,
-                   "phi": args.phi, "parallelism": "single GPU"},
+        "config": {"workload": desc, "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
+                   "phi": args.phi if op == "zgemm" else None, "parallelism": "single GPU"},
         "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
         "phase_ms": {kk: round(v, 4) for kk, v in phases.items()},
         "hbm": hbm,

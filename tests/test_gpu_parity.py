@@ -296,3 +296,93 @@ def test_zgemm_8192_sampled_vs_oracle(o2m):
     err = O.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -53)
     report("zgemm 8192^3 sampled", ratio=err["ratio"], maxrel=err["maxrel"])
     assert err["ratio"] <= 1.0
+
+
+def _sample(rng, m, n, count, lower=False):
+    ent = [(0, 0), (m - 1, n - 1), (m - 1, 0)] + ([] if lower else [(0, n - 1)])
+    while len(ent) < count:
+        i, j = int(rng.integers(0, m)), int(rng.integers(0, n))
+        if lower and i < j:
+            i, j = j, i
+        ent.append((i, j))
+    return ent
+
+
+@pytest.mark.slow
+def test_zgemm_8192_phi2_sampled(o2m):
+    """8192^3 with the wide exponent spread phi = 2 (N = 16)."""
+    m = n = k = 8192
+    sa, sb = W.config_seeds(3)
+    a = W.complex_matrix(m, k, sa + 10, dist="phi", phi=2.0)
+    b = W.complex_matrix(k, n, sb + 10, dist="phi", phi=2.0)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    ent = _sample(np.random.default_rng(9), m, n, 48)
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
+    hi, lo = O.dd_gemm(a, b, entries=ent)
+    absab = np.array([np.sum(np.abs(a[i, :]) * np.abs(b[:, j])) for i, j in ent])
+    err = O.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -53)
+    report("zgemm 8192^3 phi=2 sampled", ratio=err["ratio"], maxrel=err["maxrel"])
+    assert err["ratio"] <= 1.0
+
+
+@pytest.mark.slow
+def test_cgemm_16384_sampled(o2m):
+    """CGEMM 16384^3, U(-1,1) fp32, N = 8, on sampled entries."""
+    m = n = k = 16384
+    sa, sb = W.config_seeds(4)
+    a = W.complex_matrix(m, k, sa, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(k, n, sb, dist="uniform", dtype=np.complex64)
+    C = host(o2m.cgemm_2m(to_dev(a), to_dev(b), n_moduli=8))
+    ent = _sample(np.random.default_rng(10), m, n, 32)
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_cgemm(a, b, 8, entries=ent))
+    a64, b64 = a.astype(np.complex128), b.astype(np.complex128)
+    hi, lo = O.dd_gemm(a64, b64, entries=ent)
+    absab = np.array([np.sum(np.abs(a64[i, :]) * np.abs(b64[:, j])) for i, j in ent])
+    err = O.error_vs_reference(got.astype(np.complex128), absab, hi, lo, k, 2.0 ** -24)
+    report("cgemm 16384^3 sampled", ratio=err["ratio"], maxrel=err["maxrel"])
+    assert err["ratio"] <= 1.0
+
+
+@pytest.mark.slow
+def test_zherk_8192_sampled(o2m):
+    """HERK n = k = 8192, N(0,1), N = 16: sampled lower-triangle entries."""
+    n = k = 8192
+    sa, _ = W.config_seeds(5)
+    a = W.complex_matrix(n, k, sa)
+    C = host(o2m.zherk_2m(to_dev(a), n_moduli=16))
+    ent = _sample(np.random.default_rng(11), n, n, 48, lower=True)
+    got = np.array([C[i, j] for i, j in ent])
+    ref = O.oq_zherk(a, 16, entries=ent)
+    assert same_bits(got, ref)
+    assert all(C[i, i].imag == 0 for i in (0, 17, n - 1))
+
+
+@pytest.mark.slow
+def test_zgemm_tall_skinny_sampled(o2m):
+    """m = n = 4096, k = 65536 (N = 16): int32 headroom and the long k-loop."""
+    m, n, k = 4096, 4096, 65536
+    sa, sb = W.config_seeds(6)
+    a = W.complex_matrix(m, k, sa)
+    b = W.complex_matrix(k, n, sb)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    ent = _sample(np.random.default_rng(12), m, n, 32)
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
+    hi, lo = O.dd_gemm(a, b, entries=ent)
+    absab = np.array([np.sum(np.abs(a[i, :]) * np.abs(b[:, j])) for i, j in ent])
+    err = O.error_vs_reference(got, absab, hi, lo, k, 2.0 ** -53)
+    report("zgemm 4096x4096x65536 sampled", ratio=err["ratio"], maxrel=err["maxrel"])
+    assert err["ratio"] <= 1.0
+
+
+@pytest.mark.slow
+def test_dsyrk_4096_sampled(o2m):
+    """SYRK n = 4096, k = 8191 (odd: the zero-padded half-k HERK)."""
+    n, k = 4096, 8191
+    a = W.real_matrix(n, k, 701)
+    C = host(o2m.dsyrk_2m(to_dev(a), n_moduli=16))
+    ent = _sample(np.random.default_rng(13), n, n, 48, lower=True)
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_dsyrk(a, 16, entries=ent))
