@@ -15,9 +15,10 @@ Contents, each following the passage cited:
 * the 2M identities over integers mod m (Section 2, eqs. 2m-pre / 2m-mul /
   2m-post), with 4M and 3M (Section 1) for cross-checks;
 * the CRT with symmetric lift (Section 3.1, Algorithm 1 steps 5-6);
-* the scaling rule (Algorithm 1 step 2; the paper leaves it open, the reading
-  used is the per-row / per-column power-of-two max rule with the budget
-  below);
+* the scaling rules (Algorithm 1 step 2; the paper leaves the choice open and
+  points to the Ozaki-II literature): the per-row / per-column power-of-two
+  max rule with its budget, and a Cauchy-Schwarz (2-norm) rule with its own
+  budget;
 * Algorithm 1 step by step in exact Python integers, for tiny inputs
   (``modular_path``);
 * wrappers of the C oracle (o2m_oracle.c): exact Gaussian 4M, the exact output
@@ -154,6 +155,16 @@ def herk_plus_mod(Ar, Ai, m: int, s: int):
     return _mm((Ar + s * Ai) % m, ((Ar - s * Ai) % m).T) % m
 
 
+def her2k_plus_mod(Ar, Ai, Br, Bi, m: int, s: int):
+    """Section 5 (HER2K, sigma = tau): the two products of C = A B^H + B A^H
+    added in the residue domain, C+ = A+ B-^T + B+ A-^T (mod m) with
+    X+- = Xr +- s Xi; C- = C+^T."""
+    Ar, Ai, Br, Bi = (np.asarray(x, dtype=object) for x in (Ar, Ai, Br, Bi))
+    Ap, Am = (Ar + s * Ai) % m, (Ar - s * Ai) % m
+    Bp, Bm = (Br + s * Bi) % m, (Br - s * Bi) % m
+    return (_mm(Ap, Bm.T) + _mm(Bp, Am.T)) % m
+
+
 # ---------------------------------------------------------------------------
 # CRT and symmetric lift (Section 3.1; Algorithm 1 steps 5-6)
 # ---------------------------------------------------------------------------
@@ -207,6 +218,30 @@ def split_budget(P: int, symmetric: bool = False) -> tuple[int, int]:
     return (pA, pA) if symmetric else (pA, P - pA)
 
 
+def budget_cs(moduli, k: int, symmetric: bool = False):
+    """Shifts (qA, qB) of the Cauchy-Schwarz rule, or None if there are none.
+
+    Under that rule every quantized row of A has 2-norm at most 2^qA + r and
+    every quantized column of B at most 2^qB + r, where r = sqrt(k/2) bounds
+    the norm of the rounding error of 2k real parts (1/2 each).  By the
+    Cauchy-Schwarz inequality |Re c|, |Im c| <= |c| <= (2^qA + r)(2^qB + r),
+    so the shifts are the largest S = qA + qB (qA = floor(S/2), qB = S - qA;
+    symmetric: qA = qB = floor(S/2)) with (2^qA + R)(2^qB + R) <= (M-1)/2 -
+    floor(M/2^32), R = ceil(sqrt(k/2)), checked in exact integers."""
+    M = product(moduli)
+    hp = (M - 1) // 2 - (M >> 32)
+    k = max(int(k), 0)
+    R = 0
+    while 2 * R * R < k:
+        R += 1
+    for S in range(hp.bit_length() - 1, -1, -1):
+        qA = S // 2
+        qB = qA if symmetric else S - qA
+        if ((1 << qA) + R) * ((1 << qB) + R) <= hp:
+            return qA, qB
+    return None
+
+
 def frexp_exponent(values) -> int:
     """E with max|v| < 2^E (frexp convention); 0 when every value is zero."""
     amax = max((abs(float(v)) for v in values), default=0.0)
@@ -222,6 +257,27 @@ def frexp_exponent(values) -> int:
 
 def _round_half_even(q: Fraction) -> int:
     return round(q)  # Fraction.__round__ rounds ties to even
+
+
+def cs_exponent_exact(values) -> int:
+    """The Cauchy-Schwarz exponent G of a complex vector, in exact rationals:
+    E = frexp exponent of the largest |Re|, |Im|; U = sum over every real and
+    imaginary part v of ceil(|v| 2^(20-E))^2; d = smallest d >= 0 with
+    4^d >= U; G = E - 20 + d (a zero vector keeps 0).  Then ||v||_2 <= 2^G."""
+    vals = list(values)
+    parts = [float(v.real) for v in vals] + [float(v.imag) for v in vals]
+    E = frexp_exponent(parts)
+    U = 0
+    for v in parts:
+        q = Fraction(abs(v)) * Fraction(2) ** (20 - E)
+        u = -((-q.numerator) // q.denominator)   # ceil
+        U += u * u
+    if U == 0:
+        return E
+    d = 0
+    while 4 ** d < U:
+        d += 1
+    return E - 20 + d
 
 
 def exact_quantize(a: np.ndarray, shifts_by_row) -> tuple[list, list]:
@@ -253,10 +309,11 @@ def exact_oq_tiny(a: np.ndarray, b: np.ndarray, pA: int, pB: int) -> np.ndarray:
     return out
 
 
-def modular_path(a: np.ndarray, b: np.ndarray, n_moduli: int) -> np.ndarray:
+def modular_path(a: np.ndarray, b: np.ndarray, n_moduli: int, scaling: str = "max") -> np.ndarray:
     """Algorithm 1 ("2M Ozaki-II") step by step, exact Python integers.
 
-    1. first n_moduli 2M moduli, M = product          2. sigma, tau (max rule)
+    1. first n_moduli 2M moduli, M = product          2. sigma, tau (max or
+                                                          Cauchy-Schwarz rule)
     3. quantize to Z[i]                                4. per modulus 2M pre/mul/post
     5. CRT per component                               6. symmetric lift
     7. reconstruct c sigma_i tau_j
@@ -265,9 +322,14 @@ def modular_path(a: np.ndarray, b: np.ndarray, n_moduli: int) -> np.ndarray:
     M = product(ms)
     m, k = a.shape
     n = b.shape[1]
-    pA, pB = split_budget(budget(ms, k))
-    E = [frexp_exponent(list(a[i, :].real) + list(a[i, :].imag)) for i in range(m)]
-    F = [frexp_exponent(list(b[:, j].real) + list(b[:, j].imag)) for j in range(n)]
+    if scaling == "cs":
+        pA, pB = budget_cs(ms, k)
+        E = [cs_exponent_exact(a[i, :]) for i in range(m)]
+        F = [cs_exponent_exact(b[:, j]) for j in range(n)]
+    else:
+        pA, pB = split_budget(budget(ms, k))
+        E = [frexp_exponent(list(a[i, :].real) + list(a[i, :].imag)) for i in range(m)]
+        F = [frexp_exponent(list(b[:, j].real) + list(b[:, j].imag)) for j in range(n)]
     Ar, Ai = exact_quantize(a, [pA - e for e in E])
     Btr, Bti = exact_quantize(b.T, [pB - f for f in F])
     Br = np.asarray(Btr, dtype=object).T
@@ -307,9 +369,9 @@ def lib():
         P, I = ctypes.c_void_p, ctypes.c_int
         L.oracle_gauss_4m.argtypes = [I, I, I, P, I, P, I, P, I]
         L.oracle_gauss_4m.restype = I
-        L.oracle_exponents.argtypes = [I, I, I, P, I, P, I, P, P, P, P]
-        L.oracle_oq_gemm.argtypes = [I, I, I, P, I, P, I, I, I, P, I, I, P, P]
-        L.oracle_oq_cint.argtypes = [I, I, I, P, I, P, I, I, I, I, P, P, P]
+        L.oracle_exponents.argtypes = [I, I, I, P, I, P, I, I, P, P, P, P]
+        L.oracle_oq_gemm.argtypes = [I, I, I, P, I, P, I, I, I, I, P, I, I, P, P]
+        L.oracle_oq_cint.argtypes = [I, I, I, P, I, P, I, I, I, I, I, P, P, P]
         L.oracle_round_i128.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         L.oracle_round_i128.restype = ctypes.c_double
         L.oracle_dd_gemm.argtypes = [I, I, I, P, I, P, I, P, P, I, I, P, P]
@@ -353,18 +415,35 @@ def gauss_4m(A: np.ndarray, B: np.ndarray) -> np.ndarray:
     return C
 
 
-def exponents(a: np.ndarray, b: np.ndarray):
+_RULES = {"max": 0, "cs": 1}
+
+
+def shifts(scaling: str, moduli, k: int, symmetric: bool = False) -> tuple[int, int]:
+    """Quantization shifts (pA, pB) of the max rule or the Cauchy-Schwarz rule."""
+    if scaling == "cs":
+        q = budget_cs(moduli, k, symmetric)
+        if q is None:
+            raise ValueError(f"no Cauchy-Schwarz shifts for {len(moduli)} moduli and k={k}")
+        return q
+    if scaling != "max":
+        raise ValueError(f"unknown scaling rule {scaling!r}")
+    return split_budget(budget(moduli, k), symmetric)
+
+
+def exponents(a: np.ndarray, b: np.ndarray, scaling: str = "max"):
     """(E, E_nonfinite, F, F_nonfinite) of the C oracle."""
     a, b = _fortran_c128(a), _fortran_c128(b)
     m, k = a.shape
     n = b.shape[1]
     E = np.zeros(m, np.int32); Eb = np.zeros(m, np.int32)
     F = np.zeros(n, np.int32); Fb = np.zeros(n, np.int32)
-    lib().oracle_exponents(m, n, k, _ptr(a), m, _ptr(b), k, _ptr(E), _ptr(Eb), _ptr(F), _ptr(Fb))
+    lib().oracle_exponents(m, n, k, _ptr(a), m, _ptr(b), k, _RULES[scaling], _ptr(E), _ptr(Eb),
+                           _ptr(F), _ptr(Fb))
     return E, Eb.astype(bool), F, Fb.astype(bool)
 
 
-def oq_gemm_shifts(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries=None) -> np.ndarray:
+def oq_gemm_shifts(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries=None,
+                   scaling: str = "max") -> np.ndarray:
     """Algorithm 1's exact output for given quantization shifts (C oracle)."""
     a, b = _fortran_c128(a), _fortran_c128(b)
     m, k = a.shape
@@ -375,45 +454,74 @@ def oq_gemm_shifts(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries=None)
         C = np.zeros((m, n), dtype=np.complex128, order="F")
     else:
         C = np.zeros(ne, dtype=np.complex128)
-    lib().oracle_oq_gemm(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, _ptr(C), m, ne, _ptr(ei), _ptr(ej))
+    lib().oracle_oq_gemm(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, _RULES[scaling], _ptr(C), m, ne,
+                         _ptr(ei), _ptr(ej))
     return C
 
 
-def oq_zgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None) -> np.ndarray:
+def oq_zgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
     """ZGEMM by Algorithm 1 with the first n_moduli 2M moduli: exact output."""
-    pA, pB = split_budget(budget(moduli_2m(n_moduli), a.shape[1]))
-    return oq_gemm_shifts(a, b, pA, pB, entries)
+    pA, pB = shifts(scaling, moduli_2m(n_moduli), a.shape[1])
+    return oq_gemm_shifts(a, b, pA, pB, entries, scaling)
 
 
-def oq_cgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None) -> np.ndarray:
+def oq_cgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
     """CGEMM: fp32 inputs (exactly widened), the same algorithm, output rounded
     to fp32 (round to nearest even)."""
-    out = oq_zgemm(a.astype(np.complex128), b.astype(np.complex128), n_moduli, entries)
+    out = oq_zgemm(a.astype(np.complex128), b.astype(np.complex128), n_moduli, entries, scaling)
     return out.astype(np.complex64)
 
 
-def oq_zherk(a: np.ndarray, n_moduli: int, entries=None) -> np.ndarray:
+def oq_zherk(a: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
     """HERK C = A A^H (Section 5) through Algorithm 1 with sigma = tau: the
-    exact quantized product with pA = pB = floor(P/2).  Returns the full
+    exact quantized product with equal shifts on both sides.  Returns the full
     Hermitian matrix (callers take the lower triangle)."""
     k = a.shape[1]
-    pA, pB = split_budget(budget(moduli_2m(n_moduli), k), symmetric=True)
-    return oq_gemm_shifts(a, np.asfortranarray(np.conj(a).T), pA, pB, entries)
+    pA, pB = shifts(scaling, moduli_2m(n_moduli), k, symmetric=True)
+    return oq_gemm_shifts(a, np.asfortranarray(np.conj(a).T), pA, pB, entries, scaling)
 
 
-def oq_dsyrk(a: np.ndarray, n_moduli: int, entries=None) -> np.ndarray:
+def oq_dsyrk(a: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
     """SYRK C = A A^T (Section 5) via Z = A1 + i A2 with half the k: the exact
-    quantized product A_int A_int^T with the HERK budget of k' = ceil(k/2)
+    quantized product A_int A_int^T with the HERK shifts of k' = ceil(k/2)
     (A A^T = Re(Z Z^H) holds exactly for the quantized integers)."""
     k = a.shape[1]
     kc = (k + 1) // 2
-    pA, pB = split_budget(budget(moduli_2m(n_moduli), kc), symmetric=True)
+    pA, pB = shifts(scaling, moduli_2m(n_moduli), kc, symmetric=True)
     ac = a.astype(np.complex128)
-    out = oq_gemm_shifts(ac, np.asfortranarray(ac.T), pA, pB, entries)
+    out = oq_gemm_shifts(ac, np.asfortranarray(ac.T), pA, pB, entries, scaling)
     return out.real.copy(order="F") if entries is None else out.real.copy()
 
 
-def oq_cint(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries) -> list[tuple[int, int]]:
+def oq_zher2k(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
+    """HER2K C = A B^H + B A^H (Section 5) with sigma = tau: row i of A and
+    row i of B share one scale, so both products carry the scale
+    sigma_i sigma_j and add exactly.  C = Z W^H with Z = [A | B] and
+    W = [B | A] (inner dimension 2k): row j of W holds the entries of row j of
+    Z, so the column exponents of W^H equal the row exponents of Z.  The exact
+    quantized product with equal shifts for inner dimension 2k; returns the
+    full Hermitian matrix."""
+    k = a.shape[1]
+    pA, pB = shifts(scaling, moduli_2m(n_moduli), 2 * k, symmetric=True)
+    z = np.hstack([np.asarray(a), np.asarray(b)])
+    w = np.hstack([np.asarray(b), np.asarray(a)])
+    return oq_gemm_shifts(z, np.asfortranarray(np.conj(w).T), pA, pB, entries, scaling)
+
+
+def oq_dsyr2k(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
+    """SYR2K C = A B^T + B A^T (Section 5) as the HER2K of Z_A = A1 + i A2 and
+    Z_B = B1 + i B2 with k' = ceil(k/2): the exact quantized product
+    [A | B] [B | A]^T with the HER2K shifts of inner dimension 2k'."""
+    k = a.shape[1]
+    kc = (k + 1) // 2
+    pA, pB = shifts(scaling, moduli_2m(n_moduli), 2 * kc, symmetric=True)
+    z = np.hstack([np.asarray(a), np.asarray(b)]).astype(np.complex128)
+    w = np.hstack([np.asarray(b), np.asarray(a)]).astype(np.complex128)
+    out = oq_gemm_shifts(z, np.asfortranarray(w.T), pA, pB, entries, scaling)
+    return out.real.copy(order="F") if entries is None else out.real.copy()
+
+
+def oq_cint(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries, scaling: str = "max") -> list[tuple[int, int]]:
     """Exact integer products (Re c, Im c) of the quantized operands at the
     listed entries, as Python ints."""
     a, b = _fortran_c128(a), _fortran_c128(b)
@@ -421,7 +529,8 @@ def oq_cint(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries) -> list[tup
     n = b.shape[1]
     ne, ei, ej = _entries(entries)
     out = np.zeros((ne, 8), dtype=np.uint64)
-    lib().oracle_oq_cint(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, ne, _ptr(ei), _ptr(ej), _ptr(out))
+    lib().oracle_oq_cint(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, _RULES[scaling], ne, _ptr(ei), _ptr(ej),
+                         _ptr(out))
     res = []
     for t in range(ne):
         vals = []

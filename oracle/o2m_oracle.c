@@ -31,9 +31,13 @@
  *                   accuracy of the method is measured against (Section 6).
  *
  * Matrices are column-major, complex interleaved (re, im), with leading
- * dimensions in complex elements.  Exponent rule (the paper leaves the choice
- * of sigma, tau open, Section 3.1/3.2): E_i is the frexp exponent of the
- * largest |Re| or |Im| in row i of A (so that max < 2^E_i), 0 for a zero row;
+ * dimensions in complex elements.  Exponent rules (the paper leaves the choice
+ * of sigma, tau open, Section 3.1/3.2, pointing to norm- and max-based rules
+ * of the Ozaki-II literature):
+ *   rule 0 (max):  E_i is the frexp exponent of the largest |Re| or |Im| in
+ *                  row i of A (so that max < 2^E_i), 0 for a zero row;
+ *   rule 1 (Cauchy-Schwarz): E_i = G with the 2-norm of row i at most 2^G,
+ *                  from an exact integer sum of squares (vec_cs_exponent).
  * F_j likewise for column j of B.  A row or column holding Inf or NaN makes
  * its whole row or column of C NaN.
  */
@@ -160,6 +164,37 @@ static int vec_exponent(const double *x, long stride, int len, int *nonfinite) {
     return e;
 }
 
+/* Cauchy-Schwarz exponent of one complex vector x (rule 1).  With E its max
+   exponent (vec_exponent), every part v is bounded by u 2^(E-20) with the
+   integer u = ceil(|v| 2^(20-E)) <= 2^20 (u = 1 for a nonzero |v| whose
+   scaled value underflows: it lies in (0, 1)).  U = sum of u^2 over both
+   parts of every entry is exact (below 2^59 for len < 2^17), so
+   ||x||_2^2 <= U 4^(E-20).  With d the smallest d >= 0 such that 4^d >= U,
+   G = E - 20 + d gives ||x||_2 <= 2^G, and G is at most one above the
+   exponent of the norm itself.  A zero vector keeps E = 0. */
+static int vec_cs_exponent(const double *x, long stride, int len, int *nonfinite) {
+    const int E = vec_exponent(x, stride, len, nonfinite);
+    if (*nonfinite) return 0;
+    u128 U = 0;
+    for (int t = 0; t < len; ++t) {
+        for (int part = 0; part < 2; ++part) {
+            const double v = x[2 * (long)t * stride + part];
+            if (v == 0.0) continue;
+            double u = ceil(ldexp(fabs(v), 20 - E));
+            if (u < 1.0) u = 1.0;
+            U += (u128)((uint64_t)u * (uint64_t)u);
+        }
+    }
+    if (U == 0) return E;
+    int d = 0;
+    while (((u128)1 << (2 * d)) < U) ++d;
+    return E - 20 + d;
+}
+
+static int row_exponent(int rule, const double *x, long stride, int len, int *nonfinite) {
+    return rule == 1 ? vec_cs_exponent(x, stride, len, nonfinite) : vec_exponent(x, stride, len, nonfinite);
+}
+
 /* Quantize one complex entry: round_Z[i] componentwise, RN-even (Algorithm 1, step 3). */
 static void quantize(const double *src, int shift, qint *re, qint *im) {
     *re = to_qint(rint(ldexp(src[0], shift)));
@@ -198,17 +233,18 @@ int oracle_gauss_4m(int m, int n, int k, const int32_t *A, int lda, const int32_
 /* O-Q: exact output of Algorithm 1                                          */
 /* ------------------------------------------------------------------------ */
 
-/* Exponents of the rows of A (m x k) and columns of B (k x n). */
+/* Exponents of the rows of A (m x k) and columns of B (k x n) under rule
+   0 (max) or 1 (Cauchy-Schwarz). */
 void oracle_exponents(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
-                      int32_t *E, int32_t *Ebad, int32_t *F, int32_t *Fbad) {
+                      int rule, int32_t *E, int32_t *Ebad, int32_t *F, int32_t *Fbad) {
     for (int i = 0; i < m; ++i) {
         int bad;
-        E[i] = vec_exponent(A + 2 * (long)i, lda, k, &bad);
+        E[i] = row_exponent(rule, A + 2 * (long)i, lda, k, &bad);
         Ebad[i] = bad;
     }
     for (int j = 0; j < n; ++j) {
         int bad;
-        F[j] = vec_exponent(B + 2 * (long)j * ldb, 1, k, &bad);
+        F[j] = row_exponent(rule, B + 2 * (long)j * ldb, 1, k, &bad);
         Fbad[j] = bad;
     }
 }
@@ -222,23 +258,25 @@ static void mul_acc(acc256 *acc, i128 *fast, int use_fast, qint x, qint y, int s
 
 /*
  * C (or the listed entries of C) = Algorithm 1 applied to A (m x k), B (k x n)
- * with quantization shifts pA, pB.  n_entries < 0: the full matrix into C with
+ * with quantization shifts pA, pB and exponent rule `rule`.  n_entries < 0: the full matrix into C with
  * leading dimension ldc.  n_entries >= 0: entry t = (ei[t], ej[t]) into
  * C[2t], C[2t+1].  Also returns, if c_int_out is non-null, the exact integer
  * products as doubles rounded (same as the unscaled output) -- used by tests.
  */
 void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
-                    int pA, int pB, double *C, int ldc, int n_entries, const int32_t *ei,
+                    int pA, int pB, int rule, double *C, int ldc, int n_entries, const int32_t *ei,
                     const int32_t *ej) {
     int32_t *E = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *Eb = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *F = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
     int32_t *Fb = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
-    oracle_exponents(m, n, k, A, lda, B, ldb, E, Eb, F, Fb);
+    oracle_exponents(m, n, k, A, lda, B, ldb, rule, E, Eb, F, Fb);
 
-    /* int128 suffices when no quantized value needs a shift and
-       2k 2^(pA+pB) < 2^126 (bound on every partial sum). */
-    int use_fast = pA <= 53 && pB <= 53 && (pA + pB + 1 + (int)ceil(log2((double)k + 1)) < 126);
+    /* int128 suffices when no quantized value needs a shift (|x| < 2^53: both
+       rules keep |x| <= 2^p + sqrt(k/2) < 2^(p+1) <= 2^53 for p <= 52) and
+       every partial sum stays below 2^126 (each of the 2k products per
+       component is below 2^(pA+pB+2)). */
+    int use_fast = pA <= 52 && pB <= 52 && (pA + pB + 3 + (int)ceil(log2((double)k + 1)) < 126);
     long total = n_entries < 0 ? (long)m * n : n_entries;
 
 #pragma omp parallel
@@ -286,13 +324,13 @@ void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double 
    64-bit words per component (little-endian two's complement): for tests that
    compare residues. out has 8 words per entry (re then im). */
 void oracle_oq_cint(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
-                    int pA, int pB, int n_entries, const int32_t *ei, const int32_t *ej,
+                    int pA, int pB, int rule, int n_entries, const int32_t *ei, const int32_t *ej,
                     uint64_t *out) {
     int32_t *E = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *Eb = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *F = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
     int32_t *Fb = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
-    oracle_exponents(m, n, k, A, lda, B, ldb, E, Eb, F, Fb);
+    oracle_exponents(m, n, k, A, lda, B, ldb, rule, E, Eb, F, Fb);
 #pragma omp parallel for schedule(dynamic, 16)
     for (long t = 0; t < n_entries; ++t) {
         int i = ei[t], j = ej[t];
