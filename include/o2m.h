@@ -14,7 +14,9 @@
  *   Section 4     The 2M moduli: the greedy set {241, 233, 229, 221, 205, ...,
  *                 37, 29} (22 moduli, product ~2^152); N = 16 gives ~2^117.
  *   Section 5     HERK: C- = C+^T, so one int8 GEMM per modulus; SYRK: A A^T
- *                 = Re(Z Z^H) with Z = A1 + i A2 (half the k).
+ *                 = Re(Z Z^H) with Z = A1 + i A2 (half the k); HER2K with a
+ *                 shared row scale: C+ = A+ B-^T + B+ A-^T is one GEMM over
+ *                 [A+ | B+] and [B- | A-]; SYR2K = the half-k HER2K.
  *
  * Conventions for every call below
  *   - Matrices are column-major.  Complex matrices are interleaved (re, im);
@@ -27,13 +29,26 @@
  *     ready when the stream reaches that point.
  *   - n_moduli is N, the number of 2M moduli used (1..22); accuracy grows by
  *     about 3.7 bits per modulus and int8 GEMM work grows linearly in N.
- *   - Scaling rule (Algorithm 1 step 2): E_i = frexp exponent of the largest
- *     |Re| or |Im| in row i of A (F_j: column j of B); P = the largest integer
- *     with 2k 2^P <= (M-1)/2 - floor(M/2^32); pA = floor(P/2), pB = P - pA
- *     (HERK/SYRK: pA = pB = floor(P/2)); entries are quantized as
- *     rint(a 2^(pA - E_i)), ties to even.  The result equals the exact
- *     integer product of the quantized operands rounded to nearest fp64 and
- *     scaled by 2^(E_i + F_j - pA - pB) (CGEMM: then rounded to fp32).
+ *   - Scaling rules (Algorithm 1 step 2; the paper leaves the choice of the
+ *     power-of-two scales open).  k below is the inner dimension of the int8
+ *     GEMMs: k for GEMM/HERK, ceil(k/2) for SYRK, twice those for the rank-2k
+ *     updates.
+ *     O2M_SCALE_MAX (the plain calls): E_i = frexp exponent of the largest
+ *       |Re| or |Im| in row i of A (F_j: column j of B); P = the largest
+ *       integer with 2k 2^P <= (M-1)/2 - floor(M/2^32); pA = floor(P/2),
+ *       pB = P - pA (symmetric ops: pA = pB = floor(P/2)).
+ *     O2M_SCALE_CS (the _ex calls): E_i = the smallest G with ||row i||_2 <=
+ *       2^G as certified by U = sum over all parts v of ceil(|v| 2^(20-e))^2
+ *       (e: the max-rule exponent of the row), i.e. E_i = e - 20 +
+ *       ceil(log4 U); (pA, pB) = the largest pA + pB (split as above) with
+ *       (2^pA + R)(2^pB + R) <= (M-1)/2 - floor(M/2^32), R = ceil(sqrt(k/2)):
+ *       by the Cauchy-Schwarz inequality every |Re c|, |Im c| then stays
+ *       recoverable.  Rows with a few dominant entries keep more bits than
+ *       under the max rule.
+ *     Entries are quantized as rint(a 2^(pA - E_i)), ties to even.  The
+ *     result equals the exact integer product of the quantized operands
+ *     rounded to nearest fp64 and scaled by 2^(E_i + F_j - pA - pB) (CGEMM:
+ *     then rounded to fp32).
  *   - Rows of A or columns of B containing Inf or NaN give NaN in the
  *     corresponding rows / columns of C; zero rows or columns give +0.
  *   - m == 0 or n == 0: nothing is done.  k == 0: C is set to zero.
@@ -68,6 +83,12 @@ typedef int o2m_status;
 #define O2M_ERR_HIP (-23)       /* a HIP runtime call or kernel launch failed       */
 #define O2M_ERR_NOMEM (-24)     /* workspace allocation failed                      */
 #define O2M_ERR_SIZE (-25)      /* a padded size or plane offset exceeds the range  */
+#define O2M_ERR_SCALING (-26)   /* unknown scaling rule, or the Cauchy-Schwarz rule
+                                   has no valid shifts for this n_moduli and k      */
+
+/* scaling rules for the _ex calls */
+#define O2M_SCALE_MAX 0         /* max rule (what the plain calls use)              */
+#define O2M_SCALE_CS 1          /* Cauchy-Schwarz (2-norm) rule                     */
 
 /* device status bits, read with o2m_get_status */
 #define O2M_STATUS_OVERFLOW 1   /* gauss mode: 2k max|A_i| max|B_j| > (M-1)/2    */
@@ -98,6 +119,35 @@ o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C
 o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
                     int n_moduli, void *stream);
 
+/* HER2K, C = A B^H + B A^H, A and B n x k complex128 (Section 5).  Row i of
+   A and row i of B share one scale (sigma = tau), so the two products add in
+   the residue domain: per modulus one int8 GEMM over k' = 2k,
+   C+ = [A+ | B+] [B- | A-]^T, and C- = C+^T.  uplo 'L' or 'l': the lower
+   triangle with Im(c_ii) = 0 exactly is written.  Requires 2k <= 149130. */
+o2m_status zher2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
+                     double *C, int ldc, int n_moduli, void *stream);
+
+/* SYR2K, C = A B^T + B A^T, A and B n x k real fp64 (Section 5): the HER2K of
+   Z_A = A[:, :k'] + i A[:, k':] and Z_B likewise, k' = ceil(k/2), real part.
+   uplo 'L' or 'l': lower triangle.  Requires 2 ceil(k/2) <= 149130. */
+o2m_status dsyr2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
+                     double *C, int ldc, int n_moduli, void *stream);
+
+/* The calls above with an explicit scaling rule (O2M_SCALE_MAX or
+   O2M_SCALE_CS, see the conventions).  Same arguments otherwise. */
+o2m_status zgemm_2m_ex(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                       double *C, int ldc, int n_moduli, int scaling, void *stream);
+o2m_status cgemm_2m_ex(int m, int n, int k, const float *A, int lda, const float *B, int ldb,
+                       float *C, int ldc, int n_moduli, int scaling, void *stream);
+o2m_status zherk_2m_ex(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
+                       int n_moduli, int scaling, void *stream);
+o2m_status dsyrk_2m_ex(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
+                       int n_moduli, int scaling, void *stream);
+o2m_status zher2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
+                        double *C, int ldc, int n_moduli, int scaling, void *stream);
+o2m_status dsyr2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
+                        double *C, int ldc, int n_moduli, int scaling, void *stream);
+
 /* Exact Gaussian-integer product (Section 2): A m x k and B k x n with int32
    (re, im) pairs, C m x n with int64 (re, im) pairs.  No scaling: 2M modulo
    N moduli with N <= 8 (M < 2^63).  Exact when every entry satisfies
@@ -116,18 +166,29 @@ o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const i
 o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, const double *B,
                              int ldb, int n_moduli, int8_t *res, int32_t *E, int32_t *F,
                              void *stream);
+/* The same with an explicit scaling rule; E, F then hold that rule's exponents. */
+o2m_status zgemm_2m_residues_ex(int m, int n, int k, const double *A, int lda, const double *B,
+                                int ldb, int n_moduli, int scaling, int8_t *res, int32_t *E,
+                                int32_t *F, void *stream);
 
 /* Host-only: the first n_moduli 2M moduli (Section 4), their smallest square
    roots of -1 (Section 2) and log2 of their product.  Any pointer may be
    NULL.  Touches no GPU. */
 o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out);
 
-/* Host-only: the scaling budget P of the scaling rule above for a given
-   n_moduli and inner dimension k. */
+/* Host-only: the budget P of the max rule for a given n_moduli and inner
+   dimension k of the int8 GEMMs. */
 o2m_status o2m_budget(int n_moduli, int k, int *P_out);
 
+/* Host-only: the quantization shifts (pA, pB) a call uses.  op as for
+   o2m_workspace_bytes, k the call's own k (the SYRK split and the rank-2k
+   doubling are applied here).  Returns O2M_ERR_SCALING when the rule has no
+   valid shifts (the call would fail the same way). */
+o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, int *pB_out);
+
 /* Bytes of workspace a call needs.  op: 'z' zgemm, 'c' cgemm, 'h' zherk,
-   's' dsyrk, 'g' gauss, 'r' zgemm_2m_residues.  Touches no GPU. */
+   's' dsyrk, 'x' zher2k, 'y' dsyr2k, 'g' gauss, 'r' zgemm_2m_residues.
+   Touches no GPU. */
 size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli);
 
 /* Use caller-owned device memory (on the current device) as the workspace

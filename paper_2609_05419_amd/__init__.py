@@ -1,4 +1,4 @@
-"""2M + Ozaki-II complex GEMM / HERK / SYRK on MI355X (gfx950).
+"""2M + Ozaki-II complex GEMM / HERK / SYRK / HER2K / SYR2K on MI355X (gfx950).
 
 Thin ctypes binding over the C-ABI library ``libo2m.so`` (include/o2m.h).
 Every step of the computation runs in the library's HIP kernels; this module
@@ -18,9 +18,9 @@ import os
 import torch
 
 __all__ = [
-    "zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
-    "moduli", "budget", "workspace_bytes", "set_workspace", "get_status", "phase_timing",
-    "phase_times", "colmajor", "O2MError", "LIB_PATH",
+    "zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
+    "zgemm_2m_residues", "moduli", "budget", "shifts", "workspace_bytes", "set_workspace",
+    "get_status", "phase_timing", "phase_times", "colmajor", "O2MError", "LIB_PATH", "SCALING",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libo2m.so")
@@ -29,14 +29,25 @@ if not os.path.exists(LIB_PATH):
 
 _L = ctypes.CDLL(LIB_PATH)
 _I, _P, _D = ctypes.c_int, ctypes.c_void_p, ctypes.c_double
+_C = ctypes.c_char
 _L.zgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
 _L.cgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
-_L.zherk_2m.argtypes = [ctypes.c_char, _I, _I, _P, _I, _P, _I, _I, _P]
-_L.dsyrk_2m.argtypes = [ctypes.c_char, _I, _I, _P, _I, _P, _I, _I, _P]
+_L.zherk_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _P]
+_L.dsyrk_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _P]
+_L.zher2k_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.dsyr2k_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.zgemm_2m_ex.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.cgemm_2m_ex.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.zherk_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.dsyrk_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.zher2k_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.dsyr2k_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.gauss_gemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
 _L.zgemm_2m_residues.argtypes = [_I, _I, _I, _P, _I, _P, _I, _I, _P, _P, _P, _P]
+_L.zgemm_2m_residues_ex.argtypes = [_I, _I, _I, _P, _I, _P, _I, _I, _I, _P, _P, _P, _P]
 _L.o2m_moduli.argtypes = [_I, _P, _P, _P]
 _L.o2m_budget.argtypes = [_I, _I, _P]
+_L.o2m_shifts.argtypes = [_C, _I, _I, _I, _P, _P]
 _L.o2m_workspace_bytes.argtypes = [ctypes.c_char, _I, _I, _I, _I]
 _L.o2m_workspace_bytes.restype = ctypes.c_size_t
 _L.o2m_set_workspace.argtypes = [_P, ctypes.c_size_t]
@@ -45,12 +56,22 @@ _L.o2m_phase_timing.argtypes = [_I]
 _L.o2m_phase_times.argtypes = [_P, _I]
 _L.o2m_status_string.argtypes = [_I]
 _L.o2m_status_string.restype = ctypes.c_char_p
-for _f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
-           "o2m_moduli", "o2m_budget", "o2m_set_workspace", "o2m_get_status", "o2m_phase_timing",
-           "o2m_phase_times"):
+for _f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex",
+           "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex", "zher2k_2m_ex", "dsyr2k_2m_ex", "gauss_gemm_2m",
+           "zgemm_2m_residues", "zgemm_2m_residues_ex", "o2m_moduli", "o2m_budget", "o2m_shifts",
+           "o2m_set_workspace", "o2m_get_status", "o2m_phase_timing", "o2m_phase_times"):
     getattr(_L, _f).restype = _I
 
 STATUS_OVERFLOW = 1
+# scaling rules: "max" (per-row maximum) and "cs" (Cauchy-Schwarz, 2-norm)
+SCALING = {"max": 0, "cs": 1}
+
+
+def _rule(scaling: str) -> int:
+    try:
+        return SCALING[scaling]
+    except KeyError:
+        raise ValueError(f"unknown scaling rule {scaling!r}; expected one of {sorted(SCALING)}") from None
 
 
 class O2MError(RuntimeError):
@@ -98,51 +119,86 @@ def _check_operands(A, B, dtype):
 
 
 def zgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
-             stream=None) -> torch.Tensor:
+             stream=None, scaling: str = "max") -> torch.Tensor:
     """C = A B for complex128 A (m x k), B (k x n) by 2M + Ozaki-II."""
     _check_operands(A, B, torch.complex128)
     m, k = A.shape
     n = B.size(1)
     C = _empty_colmajor(m, n, torch.complex128, A.device) if out is None else out
-    _check(_L.zgemm_2m(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
-                       n_moduli, _stream(stream)), "zgemm_2m")
+    _check(_L.zgemm_2m_ex(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
+                          n_moduli, _rule(scaling), _stream(stream)), "zgemm_2m")
     return C
 
 
 def cgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 8, out: torch.Tensor | None = None,
-             stream=None) -> torch.Tensor:
+             stream=None, scaling: str = "max") -> torch.Tensor:
     """C = A B for complex64 A, B by 2M + Ozaki-II (result rounded to fp32)."""
     _check_operands(A, B, torch.complex64)
     m, k = A.shape
     n = B.size(1)
     C = _empty_colmajor(m, n, torch.complex64, A.device) if out is None else out
-    _check(_L.cgemm_2m(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
-                       n_moduli, _stream(stream)), "cgemm_2m")
+    _check(_L.cgemm_2m_ex(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
+                          n_moduli, _rule(scaling), _stream(stream)), "cgemm_2m")
     return C
 
 
-def zherk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+def _sym_out(out, n, dtype, device):
+    return colmajor(torch.zeros((n, n), dtype=dtype, device=device)) if out is None else out
+
+
+def zherk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None,
+             scaling: str = "max") -> torch.Tensor:
     """Lower triangle of C = A A^H (complex128 A, n x k).  The strictly upper
     triangle of a fresh output is zero-initialised; of ``out`` it is left alone."""
     if A.dtype != torch.complex128 or not A.is_cuda:
         raise TypeError("A must be a complex128 device tensor")
     n, k = A.shape
-    if out is None:
-        out = colmajor(torch.zeros((n, n), dtype=torch.complex128, device=A.device))
-    _check(_L.zherk_2m(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
-                       _stream(stream)), "zherk_2m")
+    out = _sym_out(out, n, torch.complex128, A.device)
+    _check(_L.zherk_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+                          _rule(scaling), _stream(stream)), "zherk_2m")
     return out
 
 
-def dsyrk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+def dsyrk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None,
+             scaling: str = "max") -> torch.Tensor:
     """Lower triangle of C = A A^T (float64 A, n x k) via the half-k 2M HERK."""
     if A.dtype != torch.float64 or not A.is_cuda:
         raise TypeError("A must be a float64 device tensor")
     n, k = A.shape
-    if out is None:
-        out = colmajor(torch.zeros((n, n), dtype=torch.float64, device=A.device))
-    _check(_L.dsyrk_2m(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
-                       _stream(stream)), "dsyrk_2m")
+    out = _sym_out(out, n, torch.float64, A.device)
+    _check(_L.dsyrk_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+                          _rule(scaling), _stream(stream)), "dsyrk_2m")
+    return out
+
+
+def _check_pair(A, B, dtype):
+    for name, x in (("A", A), ("B", B)):
+        if x.dtype != dtype or not x.is_cuda:
+            raise TypeError(f"{name} must be a {dtype} device tensor")
+    if A.shape != B.shape:
+        raise ValueError(f"A and B must have the same shape: {tuple(A.shape)} vs {tuple(B.shape)}")
+
+
+def zher2k_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
+              stream=None, scaling: str = "max") -> torch.Tensor:
+    """Lower triangle of C = A B^H + B A^H (complex128 A, B: n x k)."""
+    _check_pair(A, B, torch.complex128)
+    n, k = A.shape
+    out = _sym_out(out, n, torch.complex128, A.device)
+    _check(_L.zher2k_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+                           n_moduli, _rule(scaling), _stream(stream)), "zher2k_2m")
+    return out
+
+
+def dsyr2k_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
+              stream=None, scaling: str = "max") -> torch.Tensor:
+    """Lower triangle of C = A B^T + B A^T (float64 A, B: n x k) via the
+    half-k 2M HER2K."""
+    _check_pair(A, B, torch.float64)
+    n, k = A.shape
+    out = _sym_out(out, n, torch.float64, A.device)
+    _check(_L.dsyr2k_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+                           n_moduli, _rule(scaling), _stream(stream)), "dsyr2k_2m")
     return out
 
 
@@ -166,19 +222,19 @@ def gauss_gemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 4, out: torc
     return out
 
 
-def zgemm_2m_residues(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, stream=None):
+def zgemm_2m_residues(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, stream=None, scaling: str = "max"):
     """Test hook: per-modulus (Re c mod m_l, Im c mod m_l) of the quantized
     product, int8 [n_moduli, 2, n, m] (symmetric residues), and the row /
-    column exponents E (m,), F (n,)."""
+    column exponents E (m,), F (n,) of the scaling rule."""
     _check_operands(A, B, torch.complex128)
     m, k = A.shape
     n = B.size(1)
     res = torch.empty((n_moduli, 2, n, m), dtype=torch.int8, device=A.device)
     E = torch.empty(m, dtype=torch.int32, device=A.device)
     F = torch.empty(n, dtype=torch.int32, device=A.device)
-    _check(_L.zgemm_2m_residues(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), n_moduli,
-                                res.data_ptr(), E.data_ptr(), F.data_ptr(), _stream(stream)),
-           "zgemm_2m_residues")
+    _check(_L.zgemm_2m_residues_ex(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), n_moduli,
+                                   _rule(scaling), res.data_ptr(), E.data_ptr(), F.data_ptr(),
+                                   _stream(stream)), "zgemm_2m_residues")
     return res, E, F
 
 
@@ -196,6 +252,15 @@ def budget(n_moduli: int, k: int) -> int:
     P = ctypes.c_int()
     _check(_L.o2m_budget(n_moduli, k, ctypes.addressof(P)), "o2m_budget")
     return P.value
+
+
+def shifts(op: str, n_moduli: int, k: int, scaling: str = "max") -> tuple[int, int]:
+    """Quantization shifts (pA, pB) a call of kind op ('z', 'c', 'h', 's', 'x'
+    zher2k, 'y' dsyr2k, 'r') with inner dimension k uses (host only)."""
+    pA, pB = ctypes.c_int(), ctypes.c_int()
+    _check(_L.o2m_shifts(op.encode()[:1], n_moduli, k, _rule(scaling), ctypes.addressof(pA),
+                         ctypes.addressof(pB)), "o2m_shifts")
+    return pA.value, pB.value
 
 
 def workspace_bytes(op: str, m: int, n: int, k: int, n_moduli: int) -> int:

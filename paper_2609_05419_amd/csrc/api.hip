@@ -2,7 +2,8 @@
 //
 // Every call validates its arguments on the host, then enqueues on the
 // caller's stream:
-//   K1  per-row / per-column maxima and exponents      (Algorithm 1, step 2)
+//   K1  per-row / per-column maxima and exponents      (Algorithm 1, step 2;
+//       the Cauchy-Schwarz rule adds a sum-of-squares pass)
 //   K2  quantize, residues and 2M pre into int8 planes (steps 3-4, eq. 2m-pre)
 //   K3  batched int8 MFMA GEMMs, C mod m as int8       (step 4, eq. 2m-mul)
 //   K4  2M post, CRT, symmetric lift, descale          (steps 4-7, eq. 2m-post)
@@ -57,15 +58,16 @@ int floor_half(int P) { return P >= 0 ? P / 2 : -((-P + 1) / 2); }
 
 // Geometry of one call
 struct Geometry {
-    int rows_a, rows_b;       // operand rows (m and n; HERK/SYRK: n and n)
-    int k;                    // logical inner dimension
-    int a_pad, b_pad, kpad, kblocks;
+    int rows_a, rows_b;       // operand rows (m and n; HERK/SYRK/rank-2k: n and n)
+    int k;                    // inner dimension of one source (SYRK: ceil(k/2))
+    int a_pad, b_pad, kpad, kblocks;  // kblocks: of one source
+    int halves;               // 2 for rank-2k updates ([A|B] along k), else 1
     size_t plane_a, plane_b, plane_c;
-    int products;             // 2N (GEMM) or N (HERK/SYRK)
-    bool shared_planes;       // HERK/SYRK: B planes are the A- planes
+    int products;             // 2N (GEMM) or N (HERK/SYRK/rank-2k)
+    bool shared_planes;       // symmetric ops: B planes are the A- planes
 };
 
-Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym) {
+Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halves) {
     Geometry g;
     g.rows_a = rows_a;
     g.rows_b = rows_b;
@@ -74,7 +76,8 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym) {
     g.b_pad = round_up(rows_b > 0 ? rows_b : 1, kRowBlock);
     g.kpad = round_up(k > 0 ? k : 1, kStageK);
     g.kblocks = g.kpad / kStageK;
-    g.plane_a = (size_t)g.a_pad * g.kpad;
+    g.halves = halves;
+    g.plane_a = (size_t)g.a_pad * g.kpad * halves;
     g.plane_b = (size_t)g.b_pad * g.kpad;
     g.plane_c = (size_t)g.a_pad * g.b_pad;
     g.products = sym ? N : 2 * N;
@@ -83,7 +86,7 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym) {
 }
 
 struct Buffers {
-    unsigned long long *amax_a, *amax_b;
+    unsigned long long *amax_a, *amax_b, *ssq_a, *ssq_b;
     int32_t *E, *F;
     int8_t *planes_a, *planes_b, *res;
 };
@@ -93,6 +96,8 @@ size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
     Buffers t;
     t.amax_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
     t.amax_b = g.shared_planes ? t.amax_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
+    t.ssq_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
+    t.ssq_b = g.shared_planes ? t.ssq_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
     t.E = (int32_t *)c.take(sizeof(int32_t) * g.a_pad);
     t.F = g.shared_planes ? t.E : (int32_t *)c.take(sizeof(int32_t) * g.b_pad);
     t.planes_a = (int8_t *)c.take(g.plane_a * 2 * N);
@@ -164,7 +169,7 @@ void phase_mark(int phase, hipStream_t st) {
     if (g_call_slot >= 0) (void)hipEventRecord(g_events[g_call_slot][phase], st);
 }
 
-enum Op { kOpZ, kOpC, kOpH, kOpS, kOpG, kOpR };
+enum Op { kOpZ, kOpC, kOpH, kOpS, kOpG, kOpR, kOpH2, kOpS2 };
 
 struct Call {
     Op op;
@@ -173,39 +178,66 @@ struct Call {
     const void *B; int ldb;
     void *C; int ldc;
     int N;
+    int scaling;
     hipStream_t st;
     int8_t *res_out;
     int32_t *E_out, *F_out;
 };
 
+bool is_sym(Op op) { return op == kOpH || op == kOpS || op == kOpH2 || op == kOpS2; }
+bool is_rank2(Op op) { return op == kOpH2 || op == kOpS2; }
+bool is_real_split(Op op) { return op == kOpS || op == kOpS2; }  // SYRK-type: Z = A1 + i A2
+
+// Inner dimension of one source after the SYRK split, and of the int8 GEMMs.
+int source_k(Op op, int k) { return is_real_split(op) ? (k + 1) / 2 : k; }
+int gemm_k(Op op, int k) { return (is_rank2(op) ? 2 : 1) * source_k(op, k); }
+
+// Quantization shifts of the chosen rule for the inner dimension kin.
+o2m_status shifts(const ModuliTable *t, Op op, int kin, int scaling, int *pA, int *pB) {
+    const bool sym = is_sym(op);
+    if (op == kOpG) { *pA = *pB = 0; return O2M_OK; }
+    if (scaling == O2M_SCALE_CS) {
+        return budget_cs(t, kin, sym, pA, pB) ? O2M_OK : O2M_ERR_SCALING;
+    }
+    if (scaling != O2M_SCALE_MAX) return O2M_ERR_SCALING;
+    const int P = budget(t, kin);
+    *pA = floor_half(P);
+    *pB = sym ? *pA : P - *pA;
+    return O2M_OK;
+}
+
+// Every quantized value is below 2^p (max rule) or 2^p + sqrt(k/2) < 2^(p+1)
+// (Cauchy-Schwarz rule); above 2^62 the residue kernel splits it in three.
+bool wide(int scaling, int p) { return (scaling == O2M_SCALE_CS ? p + 1 : p) > 62; }
+
 o2m_status run(const Call &c) {
-    const bool sym = c.op == kOpH || c.op == kOpS;
-    const int kc = c.op == kOpS ? (c.k + 1) / 2 : c.k;
+    const bool sym = is_sym(c.op);
+    const bool two = is_rank2(c.op);
+    const bool cs = c.scaling == O2M_SCALE_CS;
+    const int kc = source_k(c.op, c.k);
     const ModuliTable *t = moduli_table(c.N);
     if (!t) return O2M_ERR_NMODULI;
-    const Geometry g = make_geometry(c.m, sym ? c.m : c.n, kc, c.N, sym);
+    int pA = 0, pB = 0;
+    o2m_status s = shifts(t, c.op, gemm_k(c.op, c.k), c.scaling, &pA, &pB);
+    if (s != O2M_OK) return s;
+    const Geometry g = make_geometry(c.m, sym ? c.m : c.n, kc, c.N, sym, two ? 2 : 1);
     if ((long)g.a_pad * g.b_pad > (1L << 40) || (long)g.a_pad / kRowBlock * (g.b_pad / kRowBlock) * g.products > 0x7FFFFFFFL)
         return O2M_ERR_SIZE;
     void *ws = nullptr;
     int *status = nullptr;
     const size_t need = carve(g, c.N, nullptr, nullptr);
-    o2m_status s = workspace(need, &ws, &status);
+    s = workspace(need, &ws, &status);
     if (s != O2M_OK) return s;
     Buffers b;
     carve(g, c.N, ws, &b);
 
-    int pA = 0, pB = 0;
-    if (c.op != kOpG) {
-        const int P = budget(t, kc);
-        pA = floor_half(P);
-        pB = sym ? pA : P - pA;
-    }
-    const ElemType et = c.op == kOpC ? kF32 : c.op == kOpG ? kI32 : c.op == kOpS ? kR64 : kF64;
+    const ElemType et = c.op == kOpC ? kF32 : c.op == kOpG ? kI32 : is_real_split(c.op) ? kR64 : kF64;
 
     phase_mark(0, c.st);
-    // ---- K1: maxima and exponents ------------------------------------------
+    // ---- K1: maxima and exponents (rank-2k: row i of A and of B share one) --
     O2M_TRY(launch_zero(b.amax_a, sizeof(unsigned long long) * g.a_pad, c.st));
     O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
+    if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
     if (!sym) {
         O2M_TRY(launch_zero(b.amax_b, sizeof(unsigned long long) * g.b_pad, c.st));
         O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
@@ -214,20 +246,39 @@ o2m_status run(const Call &c) {
         O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, c.st));
         if (!sym) O2M_TRY(launch_exponents(c.n, b.amax_b, b.F, c.st));
     }
+    if (cs) {
+        O2M_TRY(launch_zero(b.ssq_a, sizeof(unsigned long long) * g.a_pad, c.st));
+        O2M_TRY(launch_ssq(0, et, c.m, c.k, c.A, c.lda, b.E, b.ssq_a, c.st));
+        if (two) O2M_TRY(launch_ssq(0, et, c.m, c.k, c.B, c.ldb, b.E, b.ssq_a, c.st));
+        O2M_TRY(launch_cs_exponents(c.m, b.ssq_a, b.E, c.st));
+        if (!sym) {
+            O2M_TRY(launch_zero(b.ssq_b, sizeof(unsigned long long) * g.b_pad, c.st));
+            O2M_TRY(launch_ssq(1, et, c.k, c.n, c.B, c.ldb, b.F, b.ssq_b, c.st));
+            O2M_TRY(launch_cs_exponents(c.n, b.ssq_b, b.F, c.st));
+        }
+    }
     phase_mark(1, c.st);
 
     // ---- K2: residues + 2M pre ---------------------------------------------
-    PlaneGeom ga = {c.m, kc, c.k, g.a_pad, g.kblocks, g.plane_a};
-    if (c.op == kOpS) {
-        O2M_TRY(launch_residues(2, kR64, c.A, c.lda, b.E, pA, kc, ga, t->res, b.planes_a, c.st));
-    } else {
-        O2M_TRY(launch_residues(0, et, c.A, c.lda, c.op == kOpG ? nullptr : b.E, pA, 0, ga, t->res,
+    // Rank-2k: plane 2l = [A+ | B+], plane 2l+1 = [B- | A-] along k, so that
+    // one GEMM per modulus gives C+ = A+ B-^T + B+ A-^T (Section 5, HER2K).
+    const int kb = g.kblocks;
+    const int pkb = g.halves * kb;
+    const int rmode = is_real_split(c.op) ? 2 : 0;
+    const int khalf = is_real_split(c.op) ? kc : 0;
+    const int32_t *Eq = c.op == kOpG ? nullptr : b.E;
+    PlaneGeom ga = {c.m, kc, c.k, g.a_pad, kb, pkb, 0, two ? kb : 0, g.plane_a};
+    O2M_TRY(launch_residues(rmode, et, c.A, c.lda, Eq, pA, wide(c.scaling, pA), khalf, ga, t->res,
+                            b.planes_a, c.st));
+    if (two) {
+        PlaneGeom gb2 = {c.m, kc, c.k, g.a_pad, kb, pkb, kb, 0, g.plane_a};
+        O2M_TRY(launch_residues(rmode, et, c.B, c.ldb, Eq, pA, wide(c.scaling, pA), khalf, gb2, t->res,
                                 b.planes_a, c.st));
     }
     if (!sym) {
-        PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, g.kblocks, g.plane_b};
-        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, 0, gb, t->res,
-                                b.planes_b, c.st));
+        PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, kb, kb, 0, 0, g.plane_b};
+        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, wide(c.scaling, pB), 0,
+                                gb, t->res, b.planes_b, c.st));
     }
     phase_mark(2, c.st);
 
@@ -242,7 +293,7 @@ o2m_status run(const Call &c) {
     gm.c_pstride = g.plane_c;
     gm.mt = g.a_pad / kRowBlock;
     gm.nt = g.b_pad / kRowBlock;
-    gm.kblocks = g.kblocks;
+    gm.kblocks = pkb;
     gm.batch = g.products;
     gm.mod_shift = sym ? 0 : 1;
     gm.ldc = g.a_pad;
@@ -273,8 +324,8 @@ o2m_status run(const Call &c) {
     switch (c.op) {
     case kOpZ: mode = 0; break;
     case kOpC: mode = 0; ot = kF32; break;
-    case kOpH: mode = 1; break;
-    case kOpS: mode = 2; break;
+    case kOpH: case kOpH2: mode = 1; break;
+    case kOpS: case kOpS2: mode = 2; break;
     case kOpG: mode = 3; break;
     case kOpR: mode = 4; break;
     }
@@ -285,8 +336,8 @@ o2m_status run(const Call &c) {
     }
     phase_mark(4, c.st);
     if (getenv("O2M_LOG"))
-        fprintf(stderr, "o2m: op=%d m=%d n=%d k=%d N=%d log2M=%.2f pA=%d pB=%d T=%d ws=%zu\n", (int)c.op,
-                c.m, c.n, c.k, c.N, t->log2M, pA, pB, t->crt.limbs, need);
+        fprintf(stderr, "o2m: op=%d m=%d n=%d k=%d N=%d scaling=%d log2M=%.2f pA=%d pB=%d T=%d ws=%zu\n",
+                (int)c.op, c.m, c.n, c.k, c.N, c.scaling, t->log2M, pA, pB, t->crt.limbs, need);
     return O2M_OK;
 }
 
@@ -320,50 +371,135 @@ o2m_status check_sym(char uplo, int n, int k, const void *A, int lda, const void
     return O2M_OK;
 }
 
+// rank-2k: the GEMMs run over [A | B], so twice the (SYRK-split) k must fit
+o2m_status check_sym2(char uplo, int n, int k, const void *A, int lda, const void *B, int ldb, const void *C,
+                      int ldc, int N, bool split) {
+    if (uplo != 'L' && uplo != 'l') return -1;
+    if (n < 0) return -2;
+    if (k < 0) return -3;
+    if (!A && n > 0 && k > 0) return -4;
+    if (lda < (n > 1 ? n : 1)) return -5;
+    if (!B && n > 0 && k > 0) return -6;
+    if (ldb < (n > 1 ? n : 1)) return -7;
+    if (!C && n > 0) return -8;
+    if (ldc < (n > 1 ? n : 1)) return -9;
+    if (N < 1 || N > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    const long kin = 2L * (split ? (k + 1) / 2 : k);
+    if (kin > O2M_MAX_K) return O2M_ERR_KLIMIT;
+    return O2M_OK;
+}
+
+o2m_status check_scaling(int scaling) {
+    return scaling == O2M_SCALE_MAX || scaling == O2M_SCALE_CS ? O2M_OK : O2M_ERR_SCALING;
+}
+
 }  // namespace
 
 extern "C" {
 
+o2m_status zgemm_2m_ex(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                       int ldc, int n_moduli, int scaling, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
+}
+
 o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
                     int ldc, int n_moduli, void *stream) {
+    return zgemm_2m_ex(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status cgemm_2m_ex(int m, int n, int k, const float *A, int lda, const float *B, int ldb, float *C,
+                       int ldc, int n_moduli, int scaling, void *stream) {
     o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || m == 0 || n == 0) return s;
-    return run(Call{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+    return run(Call{kOpC, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
 }
 
 o2m_status cgemm_2m(int m, int n, int k, const float *A, int lda, const float *B, int ldb, float *C,
                     int ldc, int n_moduli, void *stream) {
-    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
-    if (s != O2M_OK || m == 0 || n == 0) return s;
-    return run(Call{kOpC, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+    return cgemm_2m_ex(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status zherk_2m_ex(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
+                       int scaling, void *stream) {
+    o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || n == 0) return s;
+    return run(Call{kOpH, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
 }
 
 o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
                     void *stream) {
+    return zherk_2m_ex(uplo, n, k, A, lda, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status dsyrk_2m_ex(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
+                       int scaling, void *stream) {
     o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
+    if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpH, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+    return run(Call{kOpS, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
 }
 
 o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
                     void *stream) {
-    o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
+    return dsyrk_2m_ex(uplo, n, k, A, lda, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status zher2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                        int ldc, int n_moduli, int scaling, void *stream) {
+    o2m_status s = check_sym2(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, false);
+    if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpS, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+    return run(Call{kOpH2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
+}
+
+o2m_status zher2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                     int ldc, int n_moduli, void *stream) {
+    return zher2k_2m_ex(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status dsyr2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                        int ldc, int n_moduli, int scaling, void *stream) {
+    o2m_status s = check_sym2(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, true);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || n == 0) return s;
+    return run(Call{kOpS2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
+}
+
+o2m_status dsyr2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
+                     int ldc, int n_moduli, void *stream) {
+    return dsyr2k_2m_ex(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
 }
 
 o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const int32_t *B, int ldb,
                          int64_t *C, int ldc, int n_moduli, void *stream) {
     o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, 8);
     if (s != O2M_OK || m == 0 || n == 0) return s;
-    return run(Call{kOpG, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, (hipStream_t)stream, nullptr, nullptr, nullptr});
+    return run(Call{kOpG, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr});
+}
+
+o2m_status zgemm_2m_residues_ex(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                                int n_moduli, int scaling, int8_t *res, int32_t *E, int32_t *F, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, res, m > 1 ? m : 1, n_moduli, O2M_MAX_MODULI);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    return run(Call{kOpR, m, n, k, A, lda, B, ldb, nullptr, m, n_moduli, scaling, (hipStream_t)stream, res, E, F});
 }
 
 o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
                              int n_moduli, int8_t *res, int32_t *E, int32_t *F, void *stream) {
-    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, res, m > 1 ? m : 1, n_moduli, O2M_MAX_MODULI);
-    if (s != O2M_OK || m == 0 || n == 0) return s;
-    return run(Call{kOpR, m, n, k, A, lda, B, ldb, nullptr, m, n_moduli, (hipStream_t)stream, res, E, F});
+    return zgemm_2m_residues_ex(m, n, k, A, lda, B, ldb, n_moduli, O2M_SCALE_MAX, res, E, F, stream);
 }
 
 o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out) {
@@ -385,11 +521,37 @@ o2m_status o2m_budget(int n_moduli, int k, int *P_out) {
     return O2M_OK;
 }
 
+namespace {
+bool op_of(char op, Op *out) {
+    switch (op) {
+    case 'z': *out = kOpZ; return true;
+    case 'c': *out = kOpC; return true;
+    case 'h': *out = kOpH; return true;
+    case 's': *out = kOpS; return true;
+    case 'g': *out = kOpG; return true;
+    case 'r': *out = kOpR; return true;
+    case 'x': *out = kOpH2; return true;
+    case 'y': *out = kOpS2; return true;
+    default: return false;
+    }
+}
+}  // namespace
+
+o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, int *pB_out) {
+    Op o;
+    if (!op_of(op, &o)) return -1;
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (k < 0) return -3;
+    if (!pA_out || !pB_out) return -5;
+    if (check_scaling(scaling) != O2M_OK) return O2M_ERR_SCALING;
+    return shifts(moduli_table(n_moduli), o, gemm_k(o, k), scaling, pA_out, pB_out);
+}
+
 size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli) {
-    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI || m < 0 || n < 0 || k < 0) return 0;
-    const bool sym = op == 'h' || op == 's';
-    const int kc = op == 's' ? (k + 1) / 2 : k;
-    const Geometry g = make_geometry(m, sym ? m : n, kc, n_moduli, sym);
+    Op o;
+    if (!op_of(op, &o) || n_moduli < 1 || n_moduli > O2M_MAX_MODULI || m < 0 || n < 0 || k < 0) return 0;
+    const bool sym = is_sym(o);
+    const Geometry g = make_geometry(m, sym ? m : n, source_k(o, k), n_moduli, sym, is_rank2(o) ? 2 : 1);
     return carve(g, n_moduli, nullptr, nullptr);
 }
 
@@ -447,6 +609,7 @@ const char *o2m_status_string(o2m_status s) {
     case O2M_ERR_HIP: return "HIP runtime error";
     case O2M_ERR_NOMEM: return "workspace allocation failed";
     case O2M_ERR_SIZE: return "problem too large for the tile grid";
+    case O2M_ERR_SCALING: return "unknown scaling rule, or no Cauchy-Schwarz shifts for this n_moduli and k";
     default: break;
     }
     if (s < 0 && s >= -12) return "invalid argument (BLAS position = -status)";

@@ -73,7 +73,8 @@ constexpr int kPerThread = 16;  // k entries per thread = one lane chunk of a fr
 template <int MODE, ElemType ET, bool SPLIT3, bool SCALED>
 __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, const int32_t *E,
                                                       int shift, int khalf, int kreal, int rows, int k,
-                                                      int rows_pad, int kblocks, size_t plane_bytes,
+                                                      int rows_pad, int kblocks, int plane_kblocks,
+                                                      int kofs_p, int kofs_m, size_t plane_bytes,
                                                       ResidueParams rp, int8_t *planes) {
     const int lane = threadIdx.x & 63;
     const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);   // one wave = one fragment
@@ -126,8 +127,8 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
     }
 
     // ---- residues and 2M pre per modulus (step 4, eq. 2m-pre) -------------
-    const size_t off = plane_offset(r, kk0, kblocks);
-    int8_t *dst = planes + off;
+    int8_t *dst_p = planes + plane_offset(r, kk0 + kofs_p * kStageK, plane_kblocks);
+    int8_t *dst_m = planes + plane_offset(r, kk0 + kofs_m * kStageK, plane_kblocks) + plane_bytes;
     for (int l = 0; l < rp.n; ++l) {
         const double c26 = rp.c26[l], c52 = rp.c52[l], inv = rp.inv[l];
         const double s = (double)rp.root[l];
@@ -151,23 +152,24 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
             wp[q] = pack4(bp[0], bp[1], bp[2], bp[3]);
             wm[q] = pack4(bm[0], bm[1], bm[2], bm[3]);
         }
-        *reinterpret_cast<uint4 *>(dst + (size_t)(2 * l) * plane_bytes) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
-        *reinterpret_cast<uint4 *>(dst + (size_t)(2 * l + 1) * plane_bytes) = make_uint4(wm[0], wm[1], wm[2], wm[3]);
+        *reinterpret_cast<uint4 *>(dst_p + (size_t)(2 * l) * plane_bytes) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
+        *reinterpret_cast<uint4 *>(dst_m + (size_t)(2 * l) * plane_bytes) = make_uint4(wm[0], wm[1], wm[2], wm[3]);
     }
 }
 
 }  // namespace
 
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
-                           int khalf, const PlaneGeom &g, const ResidueParams &rp, int8_t *planes,
-                           hipStream_t st) {
+                           bool wide, int khalf, const PlaneGeom &g, const ResidueParams &rp,
+                           int8_t *planes, hipStream_t st) {
     const int kreal = khalf > 0 ? g.kreal : 0;
     const long waves = (long)(g.rows_pad / kFragRows) * (long)g.kblocks;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
-    const bool split3 = shift > 62;
+    const bool split3 = wide;
 #define O2M_RES(M, T, S3, SC)                                                                    \
     residue_kernel<M, T, S3, SC><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k,     \
-                                                        g.rows_pad, g.kblocks, g.plane_bytes, rp, \
+                                                        g.rows_pad, g.kblocks, g.plane_kblocks,   \
+                                                        g.kofs_p, g.kofs_m, g.plane_bytes, rp,    \
                                                         planes)
     if (mode == 0 && et == kF64) { if (split3) O2M_RES(0, kF64, true, true); else O2M_RES(0, kF64, false, true); }
     else if (mode == 1 && et == kF64) { if (split3) O2M_RES(1, kF64, true, true); else O2M_RES(1, kF64, false, true); }

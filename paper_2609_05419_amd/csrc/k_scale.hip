@@ -7,8 +7,13 @@
 // the bit pattern is monotone in the value, and Inf/NaN patterns sit above
 // every finite one, which flags non-finite rows for free).
 //
-// Bound: HBM.  Algorithmic bytes = the matrix read once (16 B per complex
-// fp64 element).  Rows of a column-major A are strided, so a thread owns one
+// Cauchy-Schwarz rule (the paper leaves sigma, tau open and points to norm
+// based rules of the Ozaki-II literature): a second pass bounds the 2-norm of
+// every row / column by 2^G with an exact integer sum of squares of the parts
+// rounded up to 2^-20 of the row maximum (ssq_*, cs_exponents_kernel).
+//
+// Bound: HBM.  Algorithmic bytes = the matrix read once per pass (16 B per
+// complex fp64 element).  Rows of a column-major A are strided, so a thread owns one
 // row and walks a chunk of columns: every load instruction of a wave reads 64
 // consecutive rows (1 KB contiguous).  Columns of B are contiguous: a block
 // owns a chunk of one column.
@@ -52,6 +57,40 @@ template <> struct Elem<kR64> {
     }
 };
 
+// Parts of one entry for the Cauchy-Schwarz sum of squares.
+template <ElemType ET> struct Parts;
+template <> struct Parts<kF64> {
+    static constexpr int n = 2;
+    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
+        const double2 x = reinterpret_cast<const double2 *>(X)[idx];
+        v[0] = x.x; v[1] = x.y;
+    }
+};
+template <> struct Parts<kF32> {
+    static constexpr int n = 2;
+    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
+        const float2 x = reinterpret_cast<const float2 *>(X)[idx];
+        v[0] = (double)x.x; v[1] = (double)x.y;
+    }
+};
+template <> struct Parts<kR64> {
+    static constexpr int n = 1;
+    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
+        v[0] = reinterpret_cast<const double *>(X)[idx]; v[1] = 0.0;
+    }
+};
+
+// ceil(|v| 2^(20 - e))^2 for one part: |v| < 2^e, so the ceiling is at most
+// 2^20; a nonzero part whose scaled value underflows lies in (0, 1) and
+// counts as 1.
+__device__ inline unsigned long long ssq_term(double v, int e) {
+    if (v == 0.0) return 0ull;
+    double u = ceil(ldexp(fabs(v), 20 - e));
+    u = u < 1.0 ? 1.0 : u;
+    const unsigned long long q = (unsigned long long)u;
+    return q * q;
+}
+
 constexpr int kRowChunk = 64;     // columns per thread in row mode
 constexpr int kColChunk = 2048;   // rows per block in column mode
 
@@ -87,6 +126,58 @@ __global__ __launch_bounds__(256) void amax_cols(int rows, int cols, const void 
         best = o > best ? o : best;
     }
     if ((threadIdx.x & 63) == 0 && best) atomicMax(amax + c, best);
+}
+
+// Cauchy-Schwarz sums of squares (exact in uint64: at most 2 * 2^40 per entry
+// and k <= 149130 entries, below 2^59).  Same traversal as the maxima.
+template <ElemType ET>
+__global__ __launch_bounds__(256) void ssq_rows(int rows, int cols, const void *X, int ld, const int32_t *E,
+                                                unsigned long long *U) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= rows) return;
+    const int e = E[r];
+    if (e == INT32_MIN) return;
+    const int c0 = blockIdx.y * kRowChunk;
+    const int c1 = min(cols, c0 + kRowChunk);
+    unsigned long long acc = 0;
+    for (int c = c0; c < c1; ++c) {
+        double v[2];
+        Parts<ET>::get(X, (size_t)r + (size_t)c * ld, v);
+#pragma unroll
+        for (int q = 0; q < Parts<ET>::n; ++q) acc += ssq_term(v[q], e);
+    }
+    if (acc) atomicAdd(U + r, acc);
+}
+
+template <ElemType ET>
+__global__ __launch_bounds__(256) void ssq_cols(int rows, int cols, const void *X, int ld, const int32_t *E,
+                                                unsigned long long *U) {
+    const int c = blockIdx.x;
+    const int e = E[c];
+    if (e == INT32_MIN) return;  // uniform over the block
+    const int r0 = blockIdx.y * kColChunk;
+    const int r1 = min(rows, r0 + kColChunk);
+    unsigned long long acc = 0;
+    for (int r = r0 + threadIdx.x; r < r1; r += 256) {
+        double v[2];
+        Parts<ET>::get(X, (size_t)r + (size_t)c * ld, v);
+#pragma unroll
+        for (int q = 0; q < Parts<ET>::n; ++q) acc += ssq_term(v[q], e);
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if ((threadIdx.x & 63) == 0 && acc) atomicAdd(U + c, acc);
+}
+
+// E_r -> E_r - 20 + d, d = smallest d >= 0 with 4^d >= U_r, i.e.
+// d = ceil(bitlength(U_r - 1) / 2); then ||row r||_2 <= 2^(new E_r).
+__global__ void cs_exponents_kernel(int count, const unsigned long long *U, int32_t *E) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= count) return;
+    const int e = E[i];
+    const unsigned long long u = U[i];
+    if (e == INT32_MIN || u == 0) return;
+    const int bits = u == 1 ? 0 : 64 - __clzll((long long)(u - 1));
+    E[i] = e - 20 + (bits + 1) / 2;
 }
 
 __global__ void exponents_kernel(int count, const unsigned long long *amax, int32_t *E) {
@@ -141,6 +232,35 @@ hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X,
 hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st) {
     if (count <= 0) return hipSuccess;
     exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(count, amax, E);
+    return hipGetLastError();
+}
+
+hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, int ld, const int32_t *E,
+                      unsigned long long *U, hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    if (mode == 0) {
+        dim3 grid((rows + 255) / 256, (cols + kRowChunk - 1) / kRowChunk);
+        switch (et) {
+        case kF64: ssq_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        case kF32: ssq_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        case kR64: ssq_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        default: return hipErrorInvalidValue;
+        }
+    } else {
+        dim3 grid(cols, (rows + kColChunk - 1) / kColChunk);
+        switch (et) {
+        case kF64: ssq_cols<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        case kF32: ssq_cols<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        case kR64: ssq_cols<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        default: return hipErrorInvalidValue;
+        }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_cs_exponents(int count, const unsigned long long *U, int32_t *E, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    cs_exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(count, U, E);
     return hipGetLastError();
 }
 

@@ -85,6 +85,35 @@ Big big_shr(const Big &a, int bits) {
     return r;
 }
 
+Big big_shl(const Big &a, int bits) {
+    Big r;
+    if (a.zero()) return r;
+    const int ws = bits / 32, bs = bits % 32;
+    r.w.assign(ws, 0);
+    uint32_t carry = 0;
+    for (uint32_t x : a.w) {
+        r.w.push_back(bs ? (x << bs) | carry : x);
+        carry = bs ? x >> (32 - bs) : 0;
+    }
+    if (carry) r.w.push_back(carry);
+    r.trim();
+    return r;
+}
+
+Big big_add(const Big &a, const Big &b) {
+    Big r;
+    uint64_t carry = 0;
+    const size_t n = a.w.size() > b.w.size() ? a.w.size() : b.w.size();
+    for (size_t i = 0; i < n; ++i) {
+        const uint64_t t = (uint64_t)(i < a.w.size() ? a.w[i] : 0) + (i < b.w.size() ? b.w[i] : 0) + carry;
+        r.w.push_back((uint32_t)t);
+        carry = t >> 32;
+    }
+    if (carry) r.w.push_back((uint32_t)carry);
+    r.trim();
+    return r;
+}
+
 int big_bitlen(const Big &a) {
     if (a.zero()) return 0;
     return 32 * ((int)a.w.size() - 1) + (32 - __builtin_clz(a.w.back()));
@@ -264,14 +293,42 @@ const ModuliTable *moduli_table(int n) {
     return t;
 }
 
-int budget(const ModuliTable *t, int k) {
+namespace {
+// (M-1)/2 - floor(M/2^32): the largest |Re c|, |Im c| the CRT kernel recovers.
+Big recoverable(const ModuliTable *t) {
     Big M;
     M.w.assign(t->mwords, t->mwords + t->mwords_len);
     M.trim();
     uint32_t r;
     Big h = big_div_small(big_sub(M, big_from(1)), 2, &r);  // (M-1)/2
     Big margin = big_shr(M, 32);
-    Big bmax = big_cmp(h, margin) > 0 ? big_sub(h, margin) : Big();
+    return big_cmp(h, margin) > 0 ? big_sub(h, margin) : Big();
+}
+}  // namespace
+
+bool budget_cs(const ModuliTable *t, int k, bool symmetric, int *qA, int *qB) {
+    const Big hp = recoverable(t);
+    uint64_t R = 0;                                 // ceil(sqrt(k/2)): 2 R^2 >= k
+    while (2 * R * R < (uint64_t)(k > 0 ? k : 0)) ++R;
+    for (int S = big_bitlen(hp) - 1; S >= 0; --S) {
+        const int a = S / 2, b = symmetric ? a : S - a;
+        // (2^a + R)(2^b + R) = 2^(a+b) + R 2^a + R 2^b + R^2
+        Big v = big_shl(big_from(1), a + b);
+        v = big_add(v, big_shl(big_from(R), a));
+        v = big_add(v, big_shl(big_from(R), b));
+        v = big_add(v, big_from(R * R));
+        if (big_cmp(v, hp) <= 0) {
+            *qA = a;
+            *qB = b;
+            return true;
+        }
+    }
+    return false;
+}
+
+int budget(const ModuliTable *t, int k) {
+    uint32_t r;
+    Big bmax = recoverable(t);
     uint64_t two_k = 2ull * (uint64_t)(k > 0 ? k : 1);
     if (big_cmp(bmax, big_from(two_k)) >= 0) {
         Big q = big_div_small(bmax, (uint32_t)two_k, &r);

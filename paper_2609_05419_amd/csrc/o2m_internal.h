@@ -96,6 +96,10 @@ int moduli_2m(int *out, int cap);
 int root_of_minus_one(int m);
 // Largest P with 2k 2^P <= (M-1)/2 - floor(M/2^32).
 int budget(const ModuliTable *t, int k);
+// Cauchy-Schwarz shifts: the largest S = qA + qB (qA = floor(S/2), qB = S - qA;
+// symmetric: qA = qB = floor(S/2)) with (2^qA + R)(2^qB + R) <= (M-1)/2 -
+// floor(M/2^32), R = ceil(sqrt(k/2)).  False when no S >= 0 qualifies.
+bool budget_cs(const ModuliTable *t, int k, bool symmetric, int *qA, int *qB);
 
 // ---------------------------------------------------------------------------
 // Kernel launchers (each .hip file exports its own)
@@ -109,21 +113,34 @@ hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X,
                        unsigned long long *amax, hipStream_t st);
 // K1 finish: amax bits -> exponents (INT32_MIN when non-finite).
 hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st);
+// K1, Cauchy-Schwarz rule: U_r += sum over the parts v of row (mode 0) or
+// column (mode 1) r of ceil(|v| 2^(20 - E_r))^2 (exact uint64 atomics; rows
+// with E_r = INT32_MIN are skipped), then E_r += d - 20 with d the smallest
+// d >= 0 such that 4^d >= U_r (U_r = 0 leaves E_r).
+hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, int ld, const int32_t *E,
+                      unsigned long long *U, hipStream_t st);
+hipError_t launch_cs_exponents(int count, const unsigned long long *U, int32_t *E, hipStream_t st);
 
 // K2: quantize + residues + 2M pre into operand planes.
 //   mode 0: operand rows are rows of X (A, m x k), element (r, kk) at X[r + kk*ld]
 //   mode 1: operand rows are columns of X (B, k x n), element (r, kk) at X[kk + r*ld]
 //   mode 2: SYRK, X real n x k, element (r, kk) = X[r + kk*ld] + i X[r + (kk+kh)*ld]
 //   shift: quantization shift p (value scaled by 2^(p - E_r)); E may be NULL (gauss).
+//   wide: some |quantized value| may exceed 2^62 (three-way split needed).
+// Plane 2l receives X+ and plane 2l+1 receives X-; the source's k-block j
+// lands in k-block j + kofs_p of the + plane and j + kofs_m of the - plane
+// (rank-2k updates concatenate two sources along k; otherwise both are 0).
 struct PlaneGeom {
     int rows, k;         // logical sizes (SYRK: k = ceil(kreal / 2))
     int kreal;           // SYRK: columns of the real matrix
-    int rows_pad, kblocks;
-    size_t plane_bytes;  // rows_pad * kblocks * 64
+    int rows_pad, kblocks;   // kblocks: k-blocks of this source
+    int plane_kblocks;       // k-blocks of the destination planes
+    int kofs_p, kofs_m;      // k-block offsets in the + and - planes
+    size_t plane_bytes;  // rows_pad * plane_kblocks * 64
 };
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
-                           int khalf, const PlaneGeom &g, const ResidueParams &rp, int8_t *planes,
-                           hipStream_t st);
+                           bool wide, int khalf, const PlaneGeom &g, const ResidueParams &rp,
+                           int8_t *planes, hipStream_t st);
 
 // K3: batched int8 GEMM  C_p = A_p B_p^T  (both operands K-major planes), then
 // C_p mod m_(p >> mod_shift) stored as int8 (symmetric residue), column-major

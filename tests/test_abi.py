@@ -103,3 +103,57 @@ def test_argument_errors_are_reported_before_any_gpu_work(lib):
     assert lib.zherk_2m(b"L", 0, 4, None, 1, None, 1, 16, None) == 0
     lib.o2m_status_string.restype = ctypes.c_char_p
     assert b"n_moduli" in lib.o2m_status_string(-20)
+
+
+def test_new_entry_points_declared():
+    names = declared_functions()
+    for f in ("zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex", "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex",
+              "zher2k_2m_ex", "dsyr2k_2m_ex", "zgemm_2m_residues_ex", "o2m_shifts"):
+        assert f in names
+
+
+@pytest.mark.parametrize("scaling", ["max", "cs"])
+def test_shifts_match_oracle(scaling):
+    import paper_2609_05419_amd as o2m
+    for n in (1, 2, 3, 4, 8, 12, 16, 17, 20, 22):
+        ms = O.moduli_2m(n)
+        for k in (0, 1, 2, 7, 64, 1000, 8192, 16384, 65536, 74565, 149130):
+            cases = {"z": (k, False), "c": (k, False), "r": (k, False), "h": (k, True),
+                     "s": ((k + 1) // 2, True), "x": (2 * k, True), "y": (2 * ((k + 1) // 2), True)}
+            for op, (kin, sym) in cases.items():
+                try:
+                    want = O.shifts(scaling, ms, kin, sym)
+                except ValueError:
+                    want = None
+                if want is None:
+                    with pytest.raises(o2m.O2MError) as e:
+                        o2m.shifts(op, n, k, scaling)
+                    assert e.value.status == -26
+                else:
+                    assert o2m.shifts(op, n, k, scaling) == want, (op, n, k)
+
+
+def test_rank2k_and_scaling_argument_errors(lib):
+    P, I, C = ctypes.c_void_p, ctypes.c_int, ctypes.c_char
+    fake = P(0x1000)
+    lib.zher2k_2m.argtypes = [C, I, I, P, I, P, I, P, I, I, P]
+    f = lib.zher2k_2m
+    assert f(b"U", 4, 4, fake, 4, fake, 4, fake, 4, 16, None) == -1
+    assert f(b"L", -1, 4, fake, 4, fake, 4, fake, 4, 16, None) == -2
+    assert f(b"L", 4, -1, fake, 4, fake, 4, fake, 4, 16, None) == -3
+    assert f(b"L", 4, 4, None, 4, fake, 4, fake, 4, 16, None) == -4
+    assert f(b"L", 4, 4, fake, 3, fake, 4, fake, 4, 16, None) == -5
+    assert f(b"L", 4, 4, fake, 4, None, 4, fake, 4, 16, None) == -6
+    assert f(b"L", 4, 4, fake, 4, fake, 3, fake, 4, 16, None) == -7
+    assert f(b"L", 4, 4, fake, 4, fake, 4, None, 4, 16, None) == -8
+    assert f(b"L", 4, 4, fake, 4, fake, 4, fake, 3, 16, None) == -9
+    assert f(b"L", 4, 4, fake, 4, fake, 4, fake, 4, 23, None) == -20
+    assert f(b"L", 4, 74566, fake, 4, fake, 4, fake, 4, 16, None) == -21   # 2k > 149130
+    assert f(b"L", 0, 4, None, 1, None, 1, None, 1, 16, None) == 0
+    lib.dsyr2k_2m.argtypes = lib.zher2k_2m.argtypes
+    assert lib.dsyr2k_2m(b"L", 4, 149132, fake, 4, fake, 4, fake, 4, 16, None) == -21
+    lib.zgemm_2m_ex.argtypes = [I, I, I, P, I, P, I, P, I, I, I, P]
+    assert lib.zgemm_2m_ex(4, 4, 4, fake, 4, fake, 4, fake, 4, 16, 2, None) == -26
+    assert lib.zgemm_2m_ex(4, 4, 8192, fake, 4, fake, 8192, fake, 4, 1, 1, None) == -26  # no CS shifts
+    lib.o2m_status_string.restype = ctypes.c_char_p
+    assert b"scaling" in lib.o2m_status_string(-26)
