@@ -6,7 +6,8 @@ Section 6, phi = 0.5), N = 16 2M moduli (log2 M ~ 117.7), seeded synthetic
 data.  One step = one full zgemm_2m call (scaling, residues + 2M pre, the 32
 int8 GEMMs, 2M post + CRT + descale) with inputs resident in HBM.
 
-Prints ONE JSON line on stdout (diagnostics go to stderr).  The line carries
+Prints ONE JSON line on stdout (diagnostics go to stderr); only the optional
+``--sweep-n`` mode prints one line per moduli count.  The line carries
 the roofline of the dominant kernel (the batched int8 GEMM, timed live with
 HIP events recorded by the library on the call's stream), the CPU oracle timed
 on a bounded sample of the same workload, native complex128 torch.matmul on
@@ -77,7 +78,12 @@ def cpu_baseline(a, b, n_moduli, rows, cols):
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--op", choices=("zgemm", "cgemm", "zherk", "dsyrk"), default="zgemm")
+    ap.add_argument("--op", choices=("zgemm", "cgemm", "zherk", "dsyrk", "zher2k", "dsyr2k"), default="zgemm")
+    ap.add_argument("--scaling", choices=("max", "cs"), default="max",
+                    help="scaling rule: per-row maximum (default) or Cauchy-Schwarz (2-norm)")
+    ap.add_argument("--sweep-n", default="",
+                    help="comma-separated moduli counts: one JSON line per N on the same inputs "
+                         "(perf-vs-precision sweep; not the default single-line run)")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--m", type=int, default=8192)
@@ -115,8 +121,9 @@ def main() -> int:
 
     op = args.op
     m, n, k, N = args.m, args.n, args.k, args.n_moduli
-    if op in ("zherk", "dsyrk"):
+    if op in ("zherk", "dsyrk", "zher2k", "dsyr2k"):
         n = m
+    rule = args.scaling
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -124,165 +131,199 @@ def main() -> int:
     def to_dev(x):
         return torch.from_numpy(np.ascontiguousarray(x.T)).to(dev).t()
 
-    cfg = {"zgemm": 3, "cgemm": 4, "zherk": 5, "dsyrk": 5}[op]
+    cfg = {"zgemm": 3, "cgemm": 4, "zherk": 5, "dsyrk": 5, "zher2k": 5, "dsyr2k": 5}[op]
     sa, sb = workloads.config_seeds(cfg)
     log(f"bench: {op} m={m} n={n} k={k} N={N}: generating inputs")
+    b = None
     if op == "zgemm":
         a = workloads.complex_matrix(m, k, sa, dist="phi", phi=args.phi)
         b = workloads.complex_matrix(k, n, sb, dist="phi", phi=args.phi)
         A, B = to_dev(a), to_dev(b)
         C = torch.empty((n, m), dtype=torch.complex128, device=dev).t()
-        call = lambda: o2m.zgemm_2m(A, B, n_moduli=N, out=C)
-        flops, int8_ops = 8.0 * m * n * k, 4.0 * N * m * n * k
+        call = lambda N: o2m.zgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 8.0 * m * n * k, 4.0 * m * n * k
         metric = ("effective ZGEMM TFLOP/s (8mnk/t) at m=n=k=8192 + int8 MFMA util %"
                   if (m, n, k) == (8192, 8192, 8192) else "effective ZGEMM TFLOP/s (8mnk/t)")
         desc = (f"zgemm_2m {m}x{n}x{k} complex128, parts U(-0.5,0.5)*exp({args.phi}*N(0,1)), "
-                f"{N} 2M moduli, int8 MFMA")
-        pre_bytes = (16.0 + 2 * N) * (m * k + k * n)
+                "{N} 2M moduli, int8 MFMA")
+        pre_bytes = lambda N: (16.0 + 2 * N) * (m * k + k * n)
         scale_bytes = 16.0 * (m * k + k * n)
-        post_bytes = (2.0 * N + 16.0) * m * n
+        post_bytes = lambda N: (2.0 * N + 16.0) * m * n
     elif op == "cgemm":
         a = workloads.complex_matrix(m, k, sa, dist="uniform", dtype=np.complex64)
         b = workloads.complex_matrix(k, n, sb, dist="uniform", dtype=np.complex64)
         A, B = to_dev(a), to_dev(b)
         C = torch.empty((n, m), dtype=torch.complex64, device=dev).t()
-        call = lambda: o2m.cgemm_2m(A, B, n_moduli=N, out=C)
-        flops, int8_ops = 8.0 * m * n * k, 4.0 * N * m * n * k
+        call = lambda N: o2m.cgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 8.0 * m * n * k, 4.0 * m * n * k
         metric = "effective CGEMM TFLOP/s (8mnk/t)"
-        desc = f"cgemm_2m {m}x{n}x{k} complex64, parts U(-1,1), {N} 2M moduli, int8 MFMA"
-        pre_bytes = (8.0 + 2 * N) * (m * k + k * n)
+        desc = f"cgemm_2m {m}x{n}x{k} complex64, parts U(-1,1), {{N}} 2M moduli, int8 MFMA"
+        pre_bytes = lambda N: (8.0 + 2 * N) * (m * k + k * n)
         scale_bytes = 8.0 * (m * k + k * n)
-        post_bytes = (2.0 * N + 8.0) * m * n
+        post_bytes = lambda N: (2.0 * N + 8.0) * m * n
     elif op == "zherk":
         a = workloads.complex_matrix(n, k, sa)
         A = to_dev(a)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.complex128, device=dev))
-        call = lambda: o2m.zherk_2m(A, n_moduli=N, out=C)
-        flops, int8_ops = 4.0 * n * n * k, 2.0 * N * n * n * k
+        call = lambda N: o2m.zherk_2m(A, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 4.0 * n * n * k, 2.0 * n * n * k
         metric = "effective ZHERK TFLOP/s (4n^2k/t)"
-        desc = f"zherk_2m n={n} k={k} complex128 N(0,1), {N} 2M moduli, lower triangle"
-        pre_bytes = (16.0 + 2 * N) * n * k
+        desc = f"zherk_2m n={n} k={k} complex128 N(0,1), {{N}} 2M moduli, lower triangle"
+        pre_bytes = lambda N: (16.0 + 2 * N) * n * k
         scale_bytes = 16.0 * n * k
-        post_bytes = (N + 8.0) * n * n           # both triangles of C+ read, lower C written
-    else:  # dsyrk
+        post_bytes = lambda N: (N + 8.0) * n * n           # both triangles of C+ read, lower C written
+    elif op == "dsyrk":
         a = workloads.real_matrix(n, k, sa)
         A = to_dev(a)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.float64, device=dev))
-        call = lambda: o2m.dsyrk_2m(A, n_moduli=N, out=C)
-        flops, int8_ops = 1.0 * n * n * k, 2.0 * N * n * n * ((k + 1) // 2)
+        call = lambda N: o2m.dsyrk_2m(A, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 1.0 * n * n * k, 2.0 * n * n * ((k + 1) // 2)
         metric = "effective DSYRK TFLOP/s (n^2k/t)"
-        desc = f"dsyrk_2m n={n} k={k} float64 N(0,1), {N} 2M moduli, lower triangle"
-        pre_bytes = (8.0 + N) * n * k
+        desc = f"dsyrk_2m n={n} k={k} float64 N(0,1), {{N}} 2M moduli, lower triangle"
+        pre_bytes = lambda N: (8.0 + N) * n * k
         scale_bytes = 8.0 * n * k
-        post_bytes = (N + 4.0) * n * n
-    x = None
-    a_host, b_host = a, (b if op in ("zgemm", "cgemm") else None)
+        post_bytes = lambda N: (N + 4.0) * n * n
+    elif op == "zher2k":
+        a = workloads.complex_matrix(n, k, sa)
+        b = workloads.complex_matrix(n, k, sb)
+        A, B = to_dev(a), to_dev(b)
+        C = o2m.colmajor(torch.zeros((n, n), dtype=torch.complex128, device=dev))
+        call = lambda N: o2m.zher2k_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 8.0 * n * n * k, 4.0 * n * n * k   # N GEMMs n x n x 2k
+        metric = "effective ZHER2K TFLOP/s (8n^2k/t)"
+        desc = f"zher2k_2m n={n} k={k} complex128 N(0,1), {{N}} 2M moduli, lower triangle"
+        pre_bytes = lambda N: (16.0 + 2 * N) * 2 * n * k
+        scale_bytes = 16.0 * 2 * n * k
+        post_bytes = lambda N: (N + 8.0) * n * n
+    else:  # dsyr2k
+        a = workloads.real_matrix(n, k, sa)
+        b = workloads.real_matrix(n, k, sb)
+        A, B = to_dev(a), to_dev(b)
+        C = o2m.colmajor(torch.zeros((n, n), dtype=torch.float64, device=dev))
+        call = lambda N: o2m.dsyr2k_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        flops, int8_per_n = 2.0 * n * n * k, 4.0 * n * n * ((k + 1) // 2)
+        metric = "effective DSYR2K TFLOP/s (2n^2k/t)"
+        desc = f"dsyr2k_2m n={n} k={k} float64 N(0,1), {{N}} 2M moduli, lower triangle"
+        pre_bytes = lambda N: (8.0 + N) * 2 * n * k
+        scale_bytes = 8.0 * 2 * n * k
+        post_bytes = lambda N: (N + 4.0) * n * n
+    if rule == "cs":
+        scale_bytes *= 2        # the maxima pass, then the sum-of-squares pass
+        desc += ", Cauchy-Schwarz scaling"
+    a_host, b_host = a, b
 
-    log(f"bench: warmup {args.warmup}")
-    for _ in range(args.warmup):
-        call()
-    torch.cuda.synchronize()
+    def run_one(N: int, with_extras: bool) -> dict:
+        log(f"bench: N={N} warmup {args.warmup}")
+        for _ in range(args.warmup):
+            call(N)
+        torch.cuda.synchronize()
 
-    log(f"bench: timing {args.steps} steps")
-    o2m.phase_timing(True)
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        call()
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    phases = o2m.phase_times()
-    o2m.phase_timing(False)
-    log(f"bench: {ms:.3f} ms/step, phases {phases}")
+        log(f"bench: N={N} timing {args.steps} steps")
+        o2m.phase_timing(True)
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(args.steps):
+            call(N)
+        end.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / args.steps
+        phases = o2m.phase_times()
+        o2m.phase_timing(False)
+        log(f"bench: {ms:.3f} ms/step, phases {phases}")
 
-    value = flops / (ms * 1e-3) / 1e12
-    gemm_ms = phases.get("int8_gemm", float("nan"))
-    achieved = int8_ops / (gemm_ms * 1e-3) / 1e12
-    workload_key = f"{op} m{m} n{n} k{k} N{N} phi{args.phi}"
-    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_INT8_TOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
-                "traffic": load_traffic(workload_key)}
-    hbm = {
-        "scale_GBs": round(scale_bytes / (phases["scale"] * 1e-3) / 1e9, 1),
-        "residues_GBs": round(pre_bytes / (phases["residues"] * 1e-3) / 1e9, 1),
-        "crt_GBs": round(post_bytes / (phases["crt"] * 1e-3) / 1e9, 1),
-        "peak_GBs": PEAK_HBM_GBS,
-    }
+        value = flops / (ms * 1e-3) / 1e12
+        gemm_ms = phases.get("int8_gemm", float("nan"))
+        achieved = N * int8_per_n / (gemm_ms * 1e-3) / 1e12
+        workload_key = f"{op} m{m} n{n} k{k} N{N} phi{args.phi}" + ("" if rule == "max" else f" {rule}")
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_INT8_TOPS,
+                    "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
+                    "traffic": load_traffic(workload_key)}
+        hbm = {
+            "scale_GBs": round(scale_bytes / (phases["scale"] * 1e-3) / 1e9, 1),
+            "residues_GBs": round(pre_bytes(N) / (phases["residues"] * 1e-3) / 1e9, 1),
+            "crt_GBs": round(post_bytes(N) / (phases["crt"] * 1e-3) / 1e9, 1),
+            "peak_GBs": PEAK_HBM_GBS,
+        }
 
-    # sampled accuracy against the double-double reference (GEMMs)
-    accuracy = None
-    if op in ("zgemm", "cgemm"):
-        try:
-            import oracle
-            rng = np.random.default_rng(8)
-            ent = [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 64), rng.integers(0, n, 64))]
-            Ch = C.cpu().numpy()
-            got = np.array([Ch[i, j] for i, j in ent])
-            a64, b64 = a_host.astype(np.complex128), b_host.astype(np.complex128)
-            hi, lo = oracle.dd_gemm(a64, b64, entries=ent)
-            absab = np.array([np.sum(np.abs(a64[i, :]) * np.abs(b64[:, j])) for i, j in ent])
-            u = 2.0 ** -53 if op == "zgemm" else 2.0 ** -24
-            err = oracle.error_vs_reference(got.astype(np.complex128), absab, hi, lo, k, u)
-            exact = (oracle.oq_zgemm(a_host, b_host, N, entries=ent) if op == "zgemm"
-                     else oracle.oq_cgemm(a_host, b_host, N, entries=ent))
-            accuracy = {"sampled_entries": len(ent), "maxrel": err["maxrel"], "tol_ratio": err["ratio"],
-                        "bit_exact_vs_oracle": bool(np.array_equal(got, exact))}
-        except Exception as e:  # accuracy is a report, not the metric
-            log(f"bench: accuracy check skipped: {e}")
+        # sampled accuracy against the double-double reference (GEMMs)
+        accuracy = None
+        if op in ("zgemm", "cgemm"):
+            try:
+                import oracle
+                rng = np.random.default_rng(8)
+                ent = [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 64), rng.integers(0, n, 64))]
+                Ch = C.cpu().numpy()
+                got = np.array([Ch[i, j] for i, j in ent])
+                a64, b64 = a_host.astype(np.complex128), b_host.astype(np.complex128)
+                hi, lo = oracle.dd_gemm(a64, b64, entries=ent)
+                absab = np.array([np.sum(np.abs(a64[i, :]) * np.abs(b64[:, j])) for i, j in ent])
+                u = 2.0 ** -53 if op == "zgemm" else 2.0 ** -24
+                err = oracle.error_vs_reference(got.astype(np.complex128), absab, hi, lo, k, u)
+                exact = (oracle.oq_zgemm(a_host, b_host, N, entries=ent, scaling=rule) if op == "zgemm"
+                         else oracle.oq_cgemm(a_host, b_host, N, entries=ent, scaling=rule))
+                accuracy = {"sampled_entries": len(ent), "maxrel": err["maxrel"], "tol_ratio": err["ratio"],
+                            "bit_exact_vs_oracle": bool(np.array_equal(got, exact))}
+            except Exception as e:  # accuracy is a report, not the metric
+                log(f"bench: accuracy check skipped: {e}")
 
-    native = None
-    if not args.no_native and op in ("zgemm", "cgemm"):
-        try:
-            for _ in range(2):
-                Cn = torch.matmul(A, B)
-            torch.cuda.synchronize()
-            s2 = torch.cuda.Event(enable_timing=True)
-            e2 = torch.cuda.Event(enable_timing=True)
-            reps = 3
-            s2.record(stream)
-            for _ in range(reps):
-                Cn = torch.matmul(A, B)
-            e2.record(stream)
-            torch.cuda.synchronize()
-            nms = s2.elapsed_time(e2) / reps
-            native = {"op": f"torch.matmul {A.dtype}".replace("torch.", ""), "ms": round(nms, 3),
-                      "tflops": round(flops / (nms * 1e-3) / 1e12, 2)}
-            del Cn
-        except Exception as e:
-            log(f"bench: native comparison skipped: {e}")
+        native = None
+        if with_extras and not args.no_native and op in ("zgemm", "cgemm"):
+            try:
+                for _ in range(2):
+                    Cn = torch.matmul(A, B)
+                torch.cuda.synchronize()
+                s2 = torch.cuda.Event(enable_timing=True)
+                e2 = torch.cuda.Event(enable_timing=True)
+                reps = 3
+                s2.record(stream)
+                for _ in range(reps):
+                    Cn = torch.matmul(A, B)
+                e2.record(stream)
+                torch.cuda.synchronize()
+                nms = s2.elapsed_time(e2) / reps
+                native = {"op": f"torch.matmul {A.dtype}".replace("torch.", ""), "ms": round(nms, 3),
+                          "tflops": round(flops / (nms * 1e-3) / 1e12, 2)}
+                del Cn
+            except Exception as e:
+                log(f"bench: native comparison skipped: {e}")
 
-    cpu = None
-    if not args.no_cpu_baseline and op == "zgemm":
-        log("bench: CPU oracle baseline on a sample")
-        cpu = cpu_baseline(a_host, b_host, N, rows=min(m, 1536), cols=min(n, 2048))
+        cpu = None
+        if with_extras and not args.no_cpu_baseline and op == "zgemm" and rule == "max":
+            log("bench: CPU oracle baseline on a sample")
+            cpu = cpu_baseline(a_host, b_host, N, rows=min(m, 1536), cols=min(n, 2048))
 
-    line = {
-        "metric": metric,
-        "value": round(value, 2),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f64",
-        "data": "synthetic",
-        "config": {"workload": desc, "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
-                   "phi": args.phi if op == "zgemm" else None, "parallelism": "single GPU"},
-        "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
-        "phase_ms": {kk: round(v, 4) for kk, v in phases.items()},
-        "hbm": hbm,
-        "roofline": roofline,
-        "cpu_baseline": cpu,
-        "native_zgemm": native,
-        "accuracy": accuracy,
-    }
-    print(json.dumps(line), flush=True)
+        return {
+            "metric": metric,
+            "value": round(value, 2),
+            "unit": "TFLOP/s",
+            "n_gpus": 1,
+            "steps": args.steps,
+            "warmup": args.warmup,
+            "ms_per_step": round(ms, 4),
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "f64",
+            "data": "synthetic",
+            "config": {"workload": desc.format(N=N), "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
+                       "phi": args.phi if op == "zgemm" else None, "scaling_rule": rule,
+                       "parallelism": "single GPU"},
+            "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
+            "phase_ms": {kk: round(v, 4) for kk, v in phases.items()},
+            "hbm": hbm,
+            "roofline": roofline,
+            "cpu_baseline": cpu,
+            "native_zgemm": native,
+            "accuracy": accuracy,
+        }
+
+    if args.sweep_n:
+        for i, Nv in enumerate(int(x) for x in args.sweep_n.split(",")):
+            print(json.dumps(run_one(Nv, with_extras=(i == 0))), flush=True)
+        return 0
+    print(json.dumps(run_one(N, with_extras=True)), flush=True)
     return 0
 
 
