@@ -82,6 +82,23 @@ def moduli_2m(count: int | None = None) -> list[int]:
     return ms if count is None else ms[:count]
 
 
+def moduli_extension() -> list[int]:
+    """Hybrid 2M/3M moduli (Section 3.2, Section 4): once the 2M set is
+    exhausted, the greedy scan over all integers 256, 255, ..., 2 continues,
+    keeping m coprime to every 2M modulus and to every extension modulus kept
+    so far.  None of them is a 2M modulus (the 2M greedy already kept every
+    coprime one), so each is multiplied with 3M."""
+    two = moduli_2m()
+    return greedy_moduli(lambda m: all(math.gcd(m, q) == 1 for q in two))
+
+
+def moduli_set(count: int) -> list[int]:
+    """The first ``count`` moduli of Algorithm 1: the 2M set, then (hybrid) the
+    extension moduli."""
+    two = moduli_2m()
+    return two[:count] if count <= len(two) else two + moduli_extension()[:count - len(two)]
+
+
 def moduli_real() -> list[int]:
     """The real Ozaki-II set M_real (Section 4): no 2M condition."""
     return greedy_moduli(lambda m: True)
@@ -147,6 +164,17 @@ def two_m_mod(Ar, Ai, Br, Bi, m: int, s: int):
     Cp, Cm = _mm(Ap, Bp) % m, _mm(Am, Bm) % m
     h = inv2(m)
     return (h * (Cm + Cp)) % m, (s * h * (Cm - Cp)) % m
+
+
+def three_m_mod(Ar, Ai, Br, Bi, m: int):
+    """3M (Section 1) applied after reduction modulo m (Section 3.2, for the
+    moduli of a hybrid set that are not 2M moduli): T1 = Ar Br, T2 = Ai Bi,
+    T3 = (Ar + Ai)(Br + Bi), all mod m; Re C = T1 - T2, Im C = T3 - T1 - T2.
+    Returns (Re C mod m, Im C mod m) with entries in [0, m)."""
+    Ar, Ai, Br, Bi = (np.asarray(x, dtype=object) % m for x in (Ar, Ai, Br, Bi))
+    T1, T2 = _mm(Ar, Br) % m, _mm(Ai, Bi) % m
+    T3 = _mm((Ar + Ai) % m, (Br + Bi) % m) % m
+    return (T1 - T2) % m, (T3 - T1 - T2) % m
 
 
 def herk_plus_mod(Ar, Ai, m: int, s: int):
@@ -312,13 +340,14 @@ def exact_oq_tiny(a: np.ndarray, b: np.ndarray, pA: int, pB: int) -> np.ndarray:
 def modular_path(a: np.ndarray, b: np.ndarray, n_moduli: int, scaling: str = "max") -> np.ndarray:
     """Algorithm 1 ("2M Ozaki-II") step by step, exact Python integers.
 
-    1. first n_moduli 2M moduli, M = product          2. sigma, tau (max or
-                                                          Cauchy-Schwarz rule)
+    1. first n_moduli moduli, M = product              2. sigma, tau (max or
+       (2M set, then the 3M extension)                    Cauchy-Schwarz rule)
     3. quantize to Z[i]                                4. per modulus 2M pre/mul/post
+                                                          (3M for extension moduli)
     5. CRT per component                               6. symmetric lift
     7. reconstruct c sigma_i tau_j
     For tiny finite inputs only."""
-    ms = moduli_2m(n_moduli)
+    ms = moduli_set(n_moduli)
     M = product(ms)
     m, k = a.shape
     n = b.shape[1]
@@ -336,7 +365,10 @@ def modular_path(a: np.ndarray, b: np.ndarray, n_moduli: int, scaling: str = "ma
     Bi = np.asarray(Bti, dtype=object).T
     res_re, res_im = [], []
     for q in ms:
-        cr, ci = two_m_mod(Ar, Ai, Br, Bi, q, root_of(q))
+        if is_2m_modulus(q):
+            cr, ci = two_m_mod(Ar, Ai, Br, Bi, q, root_of(q))
+        else:                                   # hybrid: 3M for the extension moduli
+            cr, ci = three_m_mod(Ar, Ai, Br, Bi, q)
         res_re.append(cr)
         res_im.append(ci)
     out = np.zeros((m, n), dtype=np.complex128)
@@ -460,8 +492,9 @@ def oq_gemm_shifts(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries=None,
 
 
 def oq_zgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
-    """ZGEMM by Algorithm 1 with the first n_moduli 2M moduli: exact output."""
-    pA, pB = shifts(scaling, moduli_2m(n_moduli), a.shape[1])
+    """ZGEMM by Algorithm 1 with the first n_moduli moduli (the 2M set, then the
+    hybrid 3M extension): exact output."""
+    pA, pB = shifts(scaling, moduli_set(n_moduli), a.shape[1])
     return oq_gemm_shifts(a, b, pA, pB, entries, scaling)
 
 
@@ -477,7 +510,7 @@ def oq_zherk(a: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -
     exact quantized product with equal shifts on both sides.  Returns the full
     Hermitian matrix (callers take the lower triangle)."""
     k = a.shape[1]
-    pA, pB = shifts(scaling, moduli_2m(n_moduli), k, symmetric=True)
+    pA, pB = shifts(scaling, moduli_set(n_moduli), k, symmetric=True)
     return oq_gemm_shifts(a, np.asfortranarray(np.conj(a).T), pA, pB, entries, scaling)
 
 
@@ -487,7 +520,7 @@ def oq_dsyrk(a: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -
     (A A^T = Re(Z Z^H) holds exactly for the quantized integers)."""
     k = a.shape[1]
     kc = (k + 1) // 2
-    pA, pB = shifts(scaling, moduli_2m(n_moduli), kc, symmetric=True)
+    pA, pB = shifts(scaling, moduli_set(n_moduli), kc, symmetric=True)
     ac = a.astype(np.complex128)
     out = oq_gemm_shifts(ac, np.asfortranarray(ac.T), pA, pB, entries, scaling)
     return out.real.copy(order="F") if entries is None else out.real.copy()
@@ -502,7 +535,7 @@ def oq_zher2k(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling
     quantized product with equal shifts for inner dimension 2k; returns the
     full Hermitian matrix."""
     k = a.shape[1]
-    pA, pB = shifts(scaling, moduli_2m(n_moduli), 2 * k, symmetric=True)
+    pA, pB = shifts(scaling, moduli_set(n_moduli), 2 * k, symmetric=True)
     z = np.hstack([np.asarray(a), np.asarray(b)])
     w = np.hstack([np.asarray(b), np.asarray(a)])
     return oq_gemm_shifts(z, np.asfortranarray(np.conj(w).T), pA, pB, entries, scaling)
@@ -514,7 +547,7 @@ def oq_dsyr2k(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling
     [A | B] [B | A]^T with the HER2K shifts of inner dimension 2k'."""
     k = a.shape[1]
     kc = (k + 1) // 2
-    pA, pB = shifts(scaling, moduli_2m(n_moduli), 2 * kc, symmetric=True)
+    pA, pB = shifts(scaling, moduli_set(n_moduli), 2 * kc, symmetric=True)
     z = np.hstack([np.asarray(a), np.asarray(b)]).astype(np.complex128)
     w = np.hstack([np.asarray(b), np.asarray(a)]).astype(np.complex128)
     out = oq_gemm_shifts(z, np.asfortranarray(w.T), pA, pB, entries, scaling)
