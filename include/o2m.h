@@ -27,8 +27,15 @@
  *   - stream is a hipStream_t (NULL = the default stream).  Calls enqueue
  *     their kernels on it and return without synchronizing; the output is
  *     ready when the stream reaches that point.
- *   - n_moduli is N, the number of 2M moduli used (1..22); accuracy grows by
- *     about 3.7 bits per modulus and int8 GEMM work grows linearly in N.
+ *   - n_moduli is N, the number of moduli used; accuracy grows by about 3.7
+ *     bits per modulus and int8 GEMM work grows linearly in N.  N <= 22 uses
+ *     the 2M moduli only.  The GEMM calls (zgemm, cgemm, the residue hook)
+ *     accept N up to 32: a hybrid set (Section 3.2) where moduli 23..N are the
+ *     greedy continuation over all integers <= 256 coprime to the set
+ *     (256, 253, 251, 249, 239, 227, 223, 217, 211, 199), none a 2M modulus,
+ *     each multiplied with 3M (three int8 GEMMs: Ar Br, Ai Bi,
+ *     (Ar + Ai)(Br + Bi) mod m).  Residues mod 256 reach 128, so hybrid sets
+ *     need k <= 131071.  HERK/SYRK/rank-2k calls take N <= 22.
  *   - Scaling rules (Algorithm 1 step 2; the paper leaves the choice of the
  *     power-of-two scales open).  k below is the inner dimension of the int8
  *     GEMMs: k for GEMM/HERK, ceil(k/2) for SYRK, twice those for the rank-2k
@@ -77,8 +84,10 @@ extern "C" {
 typedef int o2m_status;
 
 #define O2M_OK 0
-#define O2M_ERR_NMODULI (-20)   /* n_moduli outside 1..22 (gauss mode: 1..8)        */
-#define O2M_ERR_KLIMIT (-21)    /* k > 149130: int32 accumulation could overflow  */
+#define O2M_ERR_NMODULI (-20)   /* n_moduli outside 1..32 (GEMM), 1..22 (symmetric
+                                   calls), 1..8 (gauss mode)                        */
+#define O2M_ERR_KLIMIT (-21)    /* k > 149130 (131071 when N > 22): int32
+                                   accumulation could overflow                      */
 #define O2M_ERR_WORKSPACE (-22) /* caller workspace too small                       */
 #define O2M_ERR_HIP (-23)       /* a HIP runtime call or kernel launch failed       */
 #define O2M_ERR_NOMEM (-24)     /* workspace allocation failed                      */
@@ -93,8 +102,10 @@ typedef int o2m_status;
 /* device status bits, read with o2m_get_status */
 #define O2M_STATUS_OVERFLOW 1   /* gauss mode: 2k max|A_i| max|B_j| > (M-1)/2    */
 
-#define O2M_MAX_MODULI 22
+#define O2M_MAX_MODULI 22          /* 2M moduli (Section 4)                        */
+#define O2M_MAX_MODULI_HYBRID 32   /* GEMM calls with the 3M extension (Section 3.2) */
 #define O2M_MAX_K 149130
+#define O2M_MAX_K_HYBRID 131071    /* k limit once N > 22 (residues mod 256)         */
 
 /* C = A B, A m x k, B k x n, complex128 (Section 3.2, Algorithm 1). */
 o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
@@ -160,7 +171,8 @@ o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const i
    (eq. 2m-post), i.e. (Re c_ij mod m_l, Im c_ij mod m_l) of the exact
    quantized product, in the symmetric range [-(m_l-1)/2, (m_l-1)/2].
    res is a device int8 array [n_moduli][2][n][m] (column-major m x n planes,
-   Re plane then Im plane per modulus); E, F (device int32, may be NULL)
+   Re plane then Im plane per modulus; for the 3M moduli of a hybrid set the
+   3M post step, Re = T1 - T2, Im = T3 - T1 - T2); E, F (device int32, may be NULL)
    receive the row / column exponents, with INT32_MIN for a non-finite row /
    column. */
 o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, const double *B,
@@ -171,9 +183,10 @@ o2m_status zgemm_2m_residues_ex(int m, int n, int k, const double *A, int lda, c
                                 int ldb, int n_moduli, int scaling, int8_t *res, int32_t *E,
                                 int32_t *F, void *stream);
 
-/* Host-only: the first n_moduli 2M moduli (Section 4), their smallest square
-   roots of -1 (Section 2) and log2 of their product.  Any pointer may be
-   NULL.  Touches no GPU. */
+/* Host-only: the first n_moduli moduli (1..32: the 2M moduli of Section 4,
+   then the hybrid 3M extension), the smallest square roots of -1 of the 2M
+   ones (Section 2; 0 for the 3M ones) and log2 of their product.  Any
+   pointer may be NULL.  Touches no GPU. */
 o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out);
 
 /* Host-only: the budget P of the max rule for a given n_moduli and inner

@@ -63,9 +63,14 @@ struct Geometry {
     int a_pad, b_pad, kpad, kblocks;  // kblocks: of one source
     int halves;               // 2 for rank-2k updates ([A|B] along k), else 1
     size_t plane_a, plane_b, plane_c;
-    int products;             // 2N (GEMM) or N (HERK/SYRK/rank-2k)
+    int products;             // int8 GEMMs: 2 per 2M modulus, 3 per 3M modulus
+                              // (GEMM), 1 per modulus (HERK/SYRK/rank-2k)
+    int planes;               // operand planes per side: products (GEMM), 2N (symmetric)
     bool shared_planes;       // symmetric ops: B planes are the A- planes
 };
+
+// 2M moduli among the first N (the rest are the 3M extension of a hybrid set)
+int count_2m(int N) { return N < kMax2M ? N : kMax2M; }
 
 Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halves) {
     Geometry g;
@@ -80,7 +85,9 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halve
     g.plane_a = (size_t)g.a_pad * g.kpad * halves;
     g.plane_b = (size_t)g.b_pad * g.kpad;
     g.plane_c = (size_t)g.a_pad * g.b_pad;
-    g.products = sym ? N : 2 * N;
+    const int n2 = count_2m(N);
+    g.products = sym ? N : 2 * n2 + 3 * (N - n2);
+    g.planes = sym ? 2 * N : g.products;
     g.shared_planes = sym;
     return g;
 }
@@ -100,8 +107,8 @@ size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
     t.ssq_b = g.shared_planes ? t.ssq_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
     t.E = (int32_t *)c.take(sizeof(int32_t) * g.a_pad);
     t.F = g.shared_planes ? t.E : (int32_t *)c.take(sizeof(int32_t) * g.b_pad);
-    t.planes_a = (int8_t *)c.take(g.plane_a * 2 * N);
-    t.planes_b = g.shared_planes ? t.planes_a : (int8_t *)c.take(g.plane_b * 2 * N);
+    t.planes_a = (int8_t *)c.take(g.plane_a * g.planes);
+    t.planes_b = g.shared_planes ? t.planes_a : (int8_t *)c.take(g.plane_b * g.planes);
     t.res = (int8_t *)c.take(g.plane_c * g.products);
     if (b) *b = t;
     return c.off;
@@ -207,8 +214,8 @@ o2m_status shifts(const ModuliTable *t, Op op, int kin, int scaling, int *pA, in
 }
 
 // Every quantized value is below 2^p (max rule) or 2^p + sqrt(k/2) < 2^(p+1)
-// (Cauchy-Schwarz rule); above 2^62 the residue kernel splits it in three.
-bool wide(int scaling, int p) { return (scaling == O2M_SCALE_CS ? p + 1 : p) > 62; }
+// (Cauchy-Schwarz rule): the residue kernel's digit count follows.
+int digits(int scaling, int p) { return residue_digits(scaling == O2M_SCALE_CS ? p + 1 : p); }
 
 o2m_status run(const Call &c) {
     const bool sym = is_sym(c.op);
@@ -268,16 +275,16 @@ o2m_status run(const Call &c) {
     const int khalf = is_real_split(c.op) ? kc : 0;
     const int32_t *Eq = c.op == kOpG ? nullptr : b.E;
     PlaneGeom ga = {c.m, kc, c.k, g.a_pad, kb, pkb, 0, two ? kb : 0, g.plane_a};
-    O2M_TRY(launch_residues(rmode, et, c.A, c.lda, Eq, pA, wide(c.scaling, pA), khalf, ga, t->res,
+    O2M_TRY(launch_residues(rmode, et, c.A, c.lda, Eq, pA, digits(c.scaling, pA), khalf, ga, t->res,
                             b.planes_a, c.st));
     if (two) {
         PlaneGeom gb2 = {c.m, kc, c.k, g.a_pad, kb, pkb, kb, 0, g.plane_a};
-        O2M_TRY(launch_residues(rmode, et, c.B, c.ldb, Eq, pA, wide(c.scaling, pA), khalf, gb2, t->res,
+        O2M_TRY(launch_residues(rmode, et, c.B, c.ldb, Eq, pA, digits(c.scaling, pA), khalf, gb2, t->res,
                                 b.planes_a, c.st));
     }
     if (!sym) {
         PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, kb, kb, 0, 0, g.plane_b};
-        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, wide(c.scaling, pB), 0,
+        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, digits(c.scaling, pB), 0,
                                 gb, t->res, b.planes_b, c.st));
     }
     phase_mark(2, c.st);
@@ -295,9 +302,13 @@ o2m_status run(const Call &c) {
     gm.nt = g.b_pad / kRowBlock;
     gm.kblocks = pkb;
     gm.batch = g.products;
-    gm.mod_shift = sym ? 0 : 1;
     gm.ldc = g.a_pad;
-    for (int l = 0; l < c.N; ++l) { gm.mod[l] = t->res.mod[l]; gm.inv[l] = t->res.inv[l]; }
+    for (int p = 0; p < g.products; ++p) {   // product -> modulus
+        const int n2 = t->res.n2;
+        const int l = sym ? p : p < 2 * n2 ? p >> 1 : n2 + (p - 2 * n2) / 3;
+        gm.mod[p] = t->res.mod[l];
+        gm.inv[p] = t->res.inv[l];
+    }
     O2M_TRY(launch_gemm(gm, c.st));
     phase_mark(3, c.st);
 
@@ -318,7 +329,10 @@ o2m_status run(const Call &c) {
     ca.amaxB = b.amax_b;
     ca.k = c.k;
     ca.status = status;
-    ca.rp = t->res;
+    for (int l = 0; l < c.N; ++l) {
+        ca.hmod[l] = (short)t->res.mod[l];
+        ca.hroot[l] = (short)t->res.root[l];
+    }
     int mode = 0;
     ElemType ot = kF64;
     switch (c.op) {
@@ -354,7 +368,7 @@ o2m_status check_gemm(int m, int n, int k, const void *A, int lda, const void *B
     if (!C && m > 0 && n > 0) return -8;
     if (ldc < (m > 1 ? m : 1)) return -9;
     if (N < 1 || N > maxN) return O2M_ERR_NMODULI;
-    if (k > O2M_MAX_K) return O2M_ERR_KLIMIT;
+    if (k > (N > O2M_MAX_MODULI ? O2M_MAX_K_HYBRID : O2M_MAX_K)) return O2M_ERR_KLIMIT;
     return O2M_OK;
 }
 
@@ -399,7 +413,7 @@ extern "C" {
 
 o2m_status zgemm_2m_ex(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
                        int ldc, int n_moduli, int scaling, void *stream) {
-    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI_HYBRID);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || m == 0 || n == 0) return s;
     return run(Call{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
@@ -413,7 +427,7 @@ o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double 
 
 o2m_status cgemm_2m_ex(int m, int n, int k, const float *A, int lda, const float *B, int ldb, float *C,
                        int ldc, int n_moduli, int scaling, void *stream) {
-    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI);
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI_HYBRID);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || m == 0 || n == 0) return s;
     return run(Call{kOpC, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
@@ -491,7 +505,7 @@ o2m_status gauss_gemm_2m(int m, int n, int k, const int32_t *A, int lda, const i
 
 o2m_status zgemm_2m_residues_ex(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
                                 int n_moduli, int scaling, int8_t *res, int32_t *E, int32_t *F, void *stream) {
-    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, res, m > 1 ? m : 1, n_moduli, O2M_MAX_MODULI);
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, res, m > 1 ? m : 1, n_moduli, O2M_MAX_MODULI_HYBRID);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || m == 0 || n == 0) return s;
     return run(Call{kOpR, m, n, k, A, lda, B, ldb, nullptr, m, n_moduli, scaling, (hipStream_t)stream, res, E, F});
@@ -503,7 +517,7 @@ o2m_status zgemm_2m_residues(int m, int n, int k, const double *A, int lda, cons
 }
 
 o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2M_out) {
-    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI_HYBRID) return O2M_ERR_NMODULI;
     const ModuliTable *t = moduli_table(n_moduli);
     for (int l = 0; l < n_moduli; ++l) {
         if (m_out) m_out[l] = t->res.mod[l];
@@ -514,7 +528,7 @@ o2m_status o2m_moduli(int n_moduli, int32_t *m_out, int32_t *s_out, double *log2
 }
 
 o2m_status o2m_budget(int n_moduli, int k, int *P_out) {
-    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI_HYBRID) return O2M_ERR_NMODULI;
     if (k < 0) return -2;
     if (!P_out) return -3;
     *P_out = budget(moduli_table(n_moduli), k);
@@ -540,7 +554,7 @@ bool op_of(char op, Op *out) {
 o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, int *pB_out) {
     Op o;
     if (!op_of(op, &o)) return -1;
-    if (n_moduli < 1 || n_moduli > O2M_MAX_MODULI) return O2M_ERR_NMODULI;
+    if (n_moduli < 1 || n_moduli > (is_sym(o) ? O2M_MAX_MODULI : O2M_MAX_MODULI_HYBRID)) return O2M_ERR_NMODULI;
     if (k < 0) return -3;
     if (!pA_out || !pB_out) return -5;
     if (check_scaling(scaling) != O2M_OK) return O2M_ERR_SCALING;
@@ -549,7 +563,8 @@ o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, in
 
 size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli) {
     Op o;
-    if (!op_of(op, &o) || n_moduli < 1 || n_moduli > O2M_MAX_MODULI || m < 0 || n < 0 || k < 0) return 0;
+    if (!op_of(op, &o) || n_moduli < 1 || m < 0 || n < 0 || k < 0) return 0;
+    if (n_moduli > (is_sym(o) ? O2M_MAX_MODULI : o == kOpG ? 8 : O2M_MAX_MODULI_HYBRID)) return 0;
     const bool sym = is_sym(o);
     const Geometry g = make_geometry(m, sym ? m : n, source_k(o, k), n_moduli, sym, is_rank2(o) ? 2 : 1);
     return carve(g, n_moduli, nullptr, nullptr);
@@ -603,8 +618,8 @@ int o2m_phase_times(float *ms, int max_phases) {
 const char *o2m_status_string(o2m_status s) {
     switch (s) {
     case O2M_OK: return "success";
-    case O2M_ERR_NMODULI: return "n_moduli out of range (1..22; gauss mode 1..8)";
-    case O2M_ERR_KLIMIT: return "k exceeds 149130 (int32 accumulation bound)";
+    case O2M_ERR_NMODULI: return "n_moduli out of range (1..32 for GEMM, 1..22 for HERK/SYRK/rank-2k, 1..8 gauss)";
+    case O2M_ERR_KLIMIT: return "k exceeds 149130 (131071 with more than 22 moduli): int32 accumulation bound";
     case O2M_ERR_WORKSPACE: return "caller workspace too small";
     case O2M_ERR_HIP: return "HIP runtime error";
     case O2M_ERR_NOMEM: return "workspace allocation failed";

@@ -52,82 +52,85 @@ O2M_HD inline double sum3_rn(double a, double b, double c) {
     return th + sum_round_odd(tl, ul);
 }
 
-// 192-bit two's complement integer, little-endian 64-bit words.
-struct U192 {
-    uint64_t w0, w1, w2;
+// Two's complement integer of W 64-bit words, little-endian.
+template <int W>
+struct UW {
+    uint64_t w[W];
 };
 
-// a += x * 2^s (modulo 2^192); s is a multiple of 40 below 192.
-O2M_HD inline void add_shifted(U192 &a, int64_t x, int s) {
+// a += x * 2^s (modulo 2^(64 W)); 0 <= s < 64 (W - 1).
+template <int W>
+O2M_HD inline void add_shifted(UW<W> &a, int64_t x, int s) {
     const uint64_t ux = (uint64_t)x;
     const uint64_t ext = (uint64_t)(x >> 63);
-    uint64_t y0, y1, y2;
-    if (s == 0) {
-        y0 = ux; y1 = ext; y2 = ext;
-    } else if (s < 64) {
-        y0 = ux << s; y1 = (ux >> (64 - s)) | (ext << s); y2 = ext;
-    } else if (s < 128) {
-        const int t = s - 64;
-        y0 = 0; y1 = ux << t; y2 = (ux >> (64 - t)) | (ext << t);
-    } else {
-        y0 = 0; y1 = 0; y2 = ux << (s - 128);
+    const int ws = s >> 6, bs = s & 63;
+    uint64_t carry = 0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+        uint64_t y;
+        if (i < ws) y = 0;
+        else if (i == ws) y = ux << bs;
+        else if (i == ws + 1) y = bs ? (ux >> (64 - bs)) | (ext << bs) : ext;
+        else y = ext;
+        const uint64_t t = a.w[i] + y;
+        const uint64_t c1 = t < y;
+        const uint64_t r = t + carry;
+        const uint64_t c2 = r < carry;
+        a.w[i] = r;
+        carry = c1 + c2;
     }
-    const uint64_t r0 = a.w0 + y0;
-    const uint64_t c0 = r0 < y0;
-    uint64_t r1 = a.w1 + y1;
-    uint64_t c1 = r1 < y1;
-    r1 += c0;
-    c1 += r1 < c0;
-    a.w0 = r0;
-    a.w1 = r1;
-    a.w2 = a.w2 + y2 + c1;
 }
 
 O2M_HD inline int clz64(uint64_t x) { return __builtin_clzll(x); }
 
-// RN of a 192-bit signed integer, ties to even, times 2^sc (one rounding).
-O2M_HD inline double round_u192(U192 v, int sc) {
-    const bool neg = (int64_t)v.w2 < 0;
+// RN of a W-word signed integer, ties to even, times 2^sc (one rounding).
+template <int W>
+O2M_HD inline double round_words(UW<W> v, int sc) {
+    const bool neg = (int64_t)v.w[W - 1] < 0;
     if (neg) {
-        v.w0 = ~v.w0; v.w1 = ~v.w1; v.w2 = ~v.w2;
-        v.w0 += 1;
-        const uint64_t c0 = v.w0 == 0;
-        v.w1 += c0;
-        v.w2 += (c0 && v.w1 == 0);
+        uint64_t carry = 1;
+#pragma unroll
+        for (int i = 0; i < W; ++i) {
+            const uint64_t t = ~v.w[i] + carry;
+            carry = carry && t == 0;
+            v.w[i] = t;
+        }
     }
-    int lz;
-    if (v.w2) lz = clz64(v.w2);
-    else if (v.w1) lz = 64 + clz64(v.w1);
-    else if (v.w0) lz = 128 + clz64(v.w0);
-    else return 0.0;
-    uint64_t h, rest;
-    if (lz >= 128) {
-        h = v.w0 << (lz - 128);
-        rest = 0;
-    } else if (lz >= 64) {
-        const int s = lz - 64;
-        h = s ? (v.w1 << s) | (v.w0 >> (64 - s)) : v.w1;
-        rest = s ? (v.w0 << s) : v.w0;
-    } else {
-        const int s = lz;
-        h = s ? (v.w2 << s) | (v.w1 >> (64 - s)) : v.w2;
-        const uint64_t n1 = s ? (v.w1 << s) | (v.w0 >> (64 - s)) : v.w1;
-        const uint64_t n0 = s ? (v.w0 << s) : v.w0;
-        rest = n1 | n0;
+    int top = -1;  // index of the most significant nonzero word
+#pragma unroll
+    for (int i = W - 1; i >= 0; --i)
+        if (top < 0 && v.w[i]) top = i;
+    if (top < 0) return 0.0;
+    const int lz = clz64(v.w[top]);
+    // h = the 64 bits below the leading one (inclusive), rest = sticky bits
+    uint64_t h = v.w[top] << lz;
+    uint64_t rest = 0;
+    if (top > 0) {
+        if (lz) h |= v.w[top - 1] >> (64 - lz);
+        rest = v.w[top - 1] << lz;
+#pragma unroll
+        for (int i = 0; i < W; ++i)
+            if (i < top - 1) rest |= v.w[i];
     }
     uint64_t mant = h >> 11;
     const uint64_t rb = h & 0x7FF;
     if (rb > 0x400 || (rb == 0x400 && (rest != 0 || (mant & 1)))) mant += 1;
-    const int top = 191 - lz;
-    const double r = ldexp((double)mant, top - 52 + sc);
+    const int msb = 64 * top + 63 - lz;  // bit index of the leading one
+    const double r = ldexp((double)mant, msb - 52 + sc);
     return neg ? -r : r;
 }
+
+// Words needed for T limbs of 40 bits with |c_t| < 2^53, plus the sign.
+template <int T>
+struct LimbWords {
+    static constexpr int value = (40 * (T - 1) + 54 + 63) / 64;
+};
 
 // Steps 5-7 for one component: limb sums S_t = sum_l u_l w_lt (exact), the
 // quotient q = rint(X / M) from a fp64 Horner sum (exact while |c| / M stays
 // below 1/2 - 2^-32), the lifted limbs c_t = S_t - q M_t (exact), and
-// RN(c) * 2^sc.  T <= 3 rounds with the three-term sum; T = 4 through a
-// 192-bit integer.
+// RN(c) * 2^sc.  T <= 3 rounds with the three-term sum; T >= 4 through a
+// multiword integer (192 bits for T = 4, 256 bits for T = 5, 6).
 template <int T>
 O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double X = S[T - 1];
@@ -140,20 +143,22 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     } else if constexpr (T == 3) {
         return ldexp(sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]), sc);
     } else {
-        U192 v = {0, 0, 0};
-        for (int t = 0; t < T; ++t) add_shifted(v, (int64_t)c[t], 40 * t);
-        return round_u192(v, sc);
+        constexpr int W = LimbWords<T>::value;
+        UW<W> v = {};
+        for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)c[t], 40 * t);
+        return round_words<W>(v, sc);
     }
 }
 
-// The exact lifted integer as 192 bits (Gaussian-integer mode).
+// The exact lifted integer (Gaussian-integer mode: M < 2^63, two limbs).
 template <int T>
-O2M_HD inline U192 lift_exact(const double (&S)[T], const double *mlimb, double inv_m) {
+O2M_HD inline UW<LimbWords<T>::value> lift_exact(const double (&S)[T], const double *mlimb, double inv_m) {
     double X = S[T - 1];
     for (int t = T - 2; t >= 0; --t) X = fma(X, kTwo40, S[t]);
     const double q = rint(X * inv_m);
-    U192 v = {0, 0, 0};
-    for (int t = 0; t < T; ++t) add_shifted(v, (int64_t)fma(-q, mlimb[t], S[t]), 40 * t);
+    constexpr int W = LimbWords<T>::value;
+    UW<W> v = {};
+    for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)fma(-q, mlimb[t], S[t]), 40 * t);
     return v;
 }
 

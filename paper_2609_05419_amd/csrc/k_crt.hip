@@ -13,8 +13,12 @@
 // |c| / M <= 1/2 - 2^-32, far from the rounding boundary, so q is exact.  The
 // lifted value c = X - q M (step 6) is then exact as limbs c_t = S_t - q M_t,
 // rounded to the nearest double, ties to even (a correctly rounded three-term
-// sum for T <= 3 limbs, a 192-bit integer for T = 4: crt_round.h), and scaled
-// by 2^(E_i + F_j - pA - pB) (step 7).
+// sum for T <= 3 limbs, a 192- or 256-bit integer for T = 4..6: crt_round.h),
+// and scaled by 2^(E_i + F_j - pA - pB) (step 7).
+//
+// Hybrid sets (Section 3.2): for the 3M moduli the GEMM left T1 = Ar Br,
+// T2 = Ai Bi, T3 = (Ar + Ai)(Br + Bi) mod m, so u = T1 - T2 and
+// v = T3 - T1 - T2 enter the same limb sums with the plain CRT weights.
 //
 // Bound: HBM.  Algorithmic bytes per output entry: 2N residues read + 16
 // written (complex fp64; 8 for complex fp32).
@@ -51,14 +55,24 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     const int8_t *base = a.res + (size_t)j * a.ldr + i0;
 
     if (MODE == 4) {
-        for (int l = 0; l < a.rp.n; ++l) {
-            const int m = a.rp.mod[l], s = a.rp.root[l], half = (m + 1) / 2;
+        for (int l = 0; l < cp.n; ++l) {
+            const int m = a.hmod[l], s = a.hroot[l], half = (m + 1) / 2;
             int8_t *out = reinterpret_cast<int8_t *>(a.c);
             for (int e = 0; e < R && i0 + e < a.m; ++e) {
-                const int rp = base[(size_t)(2 * l) * a.plane_bytes + e];
-                const int rm = base[(size_t)(2 * l + 1) * a.plane_bytes + e];
-                int re = ((half * (rm + rp)) % m + m) % m;
-                int im = ((s * ((half * (rm - rp)) % m)) % m + m) % m;
+                int re, im;
+                if (l < cp.n2) {   // 2M post (eq. 2m-post)
+                    const int rp = base[(size_t)(2 * l) * a.plane_bytes + e];
+                    const int rm = base[(size_t)(2 * l + 1) * a.plane_bytes + e];
+                    re = ((half * (rm + rp)) % m + m) % m;
+                    im = ((s * ((half * (rm - rp)) % m)) % m + m) % m;
+                } else {           // 3M post
+                    const size_t p0 = (size_t)(2 * cp.n2 + 3 * (l - cp.n2));
+                    const int t1 = base[p0 * a.plane_bytes + e];
+                    const int t2 = base[(p0 + 1) * a.plane_bytes + e];
+                    const int t3 = base[(p0 + 2) * a.plane_bytes + e];
+                    re = ((t1 - t2) % m + m) % m;
+                    im = ((t3 - t1 - t2) % m + 2 * m) % m;
+                }
                 if (re > (m - 1) / 2) re -= m;
                 if (im > (m - 1) / 2) im -= m;
                 const size_t o = (size_t)j * a.m + i0 + e;
@@ -75,7 +89,7 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
-    for (int l = 0; l < cp.n; ++l) {
+    for (int l = 0; l < cp.n2; ++l) {
         uint32_t wp[R / 4], wm[R / 4];
         if (R == 8) {
             const uint2 p2 = *reinterpret_cast<const uint2 *>(base + (size_t)(2 * l) * a.plane_bytes);
@@ -97,16 +111,33 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
             }
         }
     }
+    // 3M moduli of a hybrid set: Re = T1 - T2, Im = T3 - T1 - T2, plain weights
+    for (int l = cp.n2; l < cp.n; ++l) {
+        const size_t p0 = (size_t)(2 * cp.n2 + 3 * (l - cp.n2));
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(base + p0 * a.plane_bytes);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(base + (p0 + 1) * a.plane_bytes);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(base + (p0 + 2) * a.plane_bytes);
+#pragma unroll
+        for (int e = 0; e < R; ++e) {
+            const int t1 = sext8(w1, e & 3), t2 = sext8(w2, e & 3), t3 = sext8(w3, e & 3);
+            const double u = (double)(t1 - t2), v = (double)(t3 - t1 - t2);
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                sre[e][t] = fma(u, cp.wre[l][t], sre[e][t]);
+                sim[e][t] = fma(v, cp.wre[l][t], sim[e][t]);
+            }
+        }
+    }
 
 #pragma unroll
     for (int e = 0; e < R; ++e) {
         const int i = i0 + e;
         if (i >= a.m) break;
         if (MODE == 3) {
-            const U192 vre = lift_exact<T>(sre[e], cp.mlimb, cp.inv_m);
-            const U192 vim = lift_exact<T>(sim[e], cp.mlimb, cp.inv_m);
+            const auto vre = lift_exact<T>(sre[e], cp.mlimb, cp.inv_m);
+            const auto vim = lift_exact<T>(sim[e], cp.mlimb, cp.inv_m);
             // exact Gaussian integers: M < 2^63, fix the lift into [-h, h]
-            int64_t re = (int64_t)vre.w0, im = (int64_t)vim.w0;
+            int64_t re = (int64_t)vre.w[0], im = (int64_t)vim.w[0];
             const int64_t M = (int64_t)cp.m_lo, h = (int64_t)cp.h_lo;
             if (re > h) re -= M; else if (re < -h) re += M;
             if (im > h) im -= M; else if (im < -h) im += M;
@@ -203,6 +234,7 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
 template <int T>
 hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &cp, hipStream_t st) {
     if (mode == 1 || mode == 2) {
+        if (T > 4 || cp.n2 != cp.n) return hipErrorInvalidValue;  // symmetric ops: 2M moduli only
         const int nb = (ca.n + 31) / 32;
         const unsigned blocks = (unsigned)nb * (unsigned)nb;
         if (mode == 1) crt_sym_kernel<T, false><<<blocks, 256, 0, st>>>(ca, cp);
@@ -217,7 +249,7 @@ hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &c
     if (blocks > 0x7FFFFFFF || blocks4 > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (mode == 0 && ot == kF64) crt_kernel<T, 0, kF64, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
     else if (mode == 0 && ot == kF32) crt_kernel<T, 0, kF32, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 3) crt_kernel<T, 3, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
+    else if (mode == 3 && T == 2) crt_kernel<2, 3, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
     else if (mode == 4) crt_kernel<T, 4, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
     else return hipErrorInvalidValue;
     return hipGetLastError();
@@ -231,6 +263,8 @@ hipError_t launch_crt(int mode, ElemType out_type, const CrtArgs &ca, const CrtP
     case 2: return launch_t<2>(mode, out_type, ca, cp, st);
     case 3: return launch_t<3>(mode, out_type, ca, cp, st);
     case 4: return launch_t<4>(mode, out_type, ca, cp, st);
+    case 5: return launch_t<5>(mode, out_type, ca, cp, st);
+    case 6: return launch_t<6>(mode, out_type, ca, cp, st);
     default: return hipErrorInvalidValue;
     }
 }

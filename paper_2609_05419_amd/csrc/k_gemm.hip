@@ -3,11 +3,12 @@
 //   C_p = A_p B_p^T   (A_p: m_pad x k_pad, B_p: n_pad x k_pad, both K-major
 //                      int8 planes in fragment order, see o2m_internal.h)
 //
-// with exact int32 accumulation: |entries| <= 120, so |C| <= 14400 k < 2^31
-// for k <= 149130.  The epilogue reduces C_p modulo m_(p >> mod_shift) to the
-// symmetric residue and stores it as int8, column-major with leading dimension
-// ldc (= m_pad), so the CRT kernel reads 1 byte per product per output entry
-// instead of 4.
+// with exact int32 accumulation: |entries| <= 120 for the 2M moduli, so
+// |C| <= 14400 k < 2^31 for k <= 149130 (<= 128 and k <= 131071 once the 3M
+// modulus 256 of a hybrid set is in).  The epilogue reduces C_p modulo the
+// product's modulus m_p to the symmetric residue and stores it as int8,
+// column-major with leading dimension ldc (= m_pad), so the CRT kernel reads
+// 1 byte per product per output entry instead of 4.
 //
 // Tiling for gfx950: a 256 x 256 output tile per workgroup of 8 waves (2 per
 // SIMD, 2 x 4), each wave owning 128 x 64 = 8 x 4 accumulators of
@@ -215,9 +216,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     // v_mfma_i32_16x16x64_i8 leaves column (lane % 16), rows 4 (lane / 16) + e
     // of its 16 x 16 block in element e: 4 consecutive rows make one dword.
     stage_barrier();  // every wave is done with the ring; no loads are in flight
-    const int mi = p >> g.mod_shift;
-    const double inv = g.inv[mi];
-    const uint32_t negm = (uint32_t)(-g.mod[mi]) & 0xFFFFFFu;
+    const double inv = g.inv[p];
+    const uint32_t negm = (uint32_t)(-g.mod[p]) & 0xFFFFFFu;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
 #pragma unroll

@@ -6,15 +6,22 @@
 // root s_l, the kernel writes the two int8 residues
 //     A+ = (x_re + s x_im) mod m,   A- = (x_re - s x_im) mod m      (eq. 2m-pre)
 // in the symmetric range [-(m-1)/2, (m-1)/2] into the operand planes 2l and
-// 2l+1, in the fragment order the int8 GEMM consumes (o2m_internal.h).
+// 2l+1, in the fragment order the int8 GEMM consumes (o2m_internal.h).  For
+// the 3M moduli of a hybrid set it writes x_re, x_im and x_re + x_im mod m
+// into three planes (3M after reduction, Section 3.2); for even m = 256 the
+// low byte of the residue in [-128, 128] is the int8 residue (-128 = 128).
 //
 // Exact residues without integer division: x (an integer held exactly in a
-// double, |x| <= 2^pA) is split as x = x2 2^52 + x1 2^26 + x0 with
-// |x1|, |x0| <= 2^25; then R = c52 x2 + c26 x1 + x0 = x (mod m) with
-// c = 2^26, 2^52 mod m (symmetric), likewise I for x_im, and A+- = R +- s I is
-// an exact integer below 2^52.  q = rint(A / m) comes out of one fma against
-// 1.5 2^52 (the low word of the sum is q), and A - q m, needed only modulo
-// 2^8, is one 24-bit integer multiply-add on the low words.
+// double) is split into D base-2^26 digits x = sum_d x_d 2^(26 d), peeled
+// from the top so that |x_d| <= 2^25 below the top digit; then
+// R = sum_d c_d x_d = x (mod m) with c_d = 2^(26 d) mod m (symmetric),
+// likewise I for x_im.  The host picks D from the bound on |x| so that the top
+// digit stays below 2^36 (D = 2 up to 2^62, 3 up to 2^88; D = 4, 5 keep it
+// below 2^30 and hold the digits as int32), which keeps |R| < 2^43.01 and
+// A+- = R +- s I an exact integer below 2^51 (s <= 120).  q = rint(A / m)
+// comes out of one fma against 1.5 2^52 (the low word of the sum is q), and
+// A - q m, needed only modulo 2^8, is one 24-bit integer multiply-add on the
+// low words.
 //
 // Bound: HBM.  Algorithmic bytes per complex fp64 input element:
 // 16 read + 2N written (8 + 2N for fp32 input).
@@ -24,10 +31,23 @@ namespace o2m {
 namespace {
 
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
-constexpr double kTwo26 = 67108864.0;
-constexpr double kTwoM26 = 1.0 / 67108864.0;
-constexpr double kTwo52 = 4503599627370496.0;
-constexpr double kTwoM52 = 1.0 / 4503599627370496.0;
+
+// Digit storage: exact doubles for D <= 3, int32 for D >= 4 (digits < 2^30).
+template <int D> struct Digit { typedef double type; };
+template <> struct Digit<4> { typedef int type; };
+template <> struct Digit<5> { typedef int type; };
+
+// x = sum_d dg[d] 2^(26 d), peeled from the top digit down (each step exact).
+template <int D, typename DT>
+__device__ inline void split_digits(double x, DT (&dg)[D][16], int e) {
+#pragma unroll
+    for (int d = D - 1; d >= 1; --d) {
+        const double q = rint(ldexp(x, -26 * d));
+        x = fma(-q, ldexp(1.0, 26 * d), x);
+        dg[d][e] = (DT)q;
+    }
+    dg[0][e] = (DT)x;
+}
 
 template <ElemType ET> struct Load;
 template <> struct Load<kF64> {
@@ -69,8 +89,8 @@ constexpr int kPerThread = 16;  // k entries per thread = one lane chunk of a fr
 // MODE 0: rows of X (A, column-major m x k): entry (r, kk) at X[r + kk*ld]
 // MODE 1: columns of X (B, column-major k x n): entry (r, kk) at X[kk + r*ld]
 // MODE 2: SYRK, X real column-major n x k: (r, kk) = X[r + kk ld] + i X[r + (kk+kh) ld]
-// SPLIT3: quantized values may exceed 2^62 (three-way split needed)
-template <int MODE, ElemType ET, bool SPLIT3, bool SCALED>
+// D: base-2^26 digits of the quantized values (2..5, from their bound)
+template <int MODE, ElemType ET, int D, bool SCALED>
 __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, const int32_t *E,
                                                       int shift, int khalf, int kreal, int rows, int k,
                                                       int rows_pad, int kblocks, int plane_kblocks,
@@ -88,8 +108,8 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
     const int kk0 = fk * kStageK + (lane >> 4) * 16;
 
     // ---- load and quantize (step 3) -------------------------------------
-    double x1r[kPerThread], x0r[kPerThread], x1i[kPerThread], x0i[kPerThread];
-    double x2r[SPLIT3 ? kPerThread : 1], x2i[SPLIT3 ? kPerThread : 1];
+    typedef typename Digit<D>::type DT;
+    DT xr[D][kPerThread], xi[D][kPerThread];
     int sh = 0;
     bool live = r < rows;
     if (SCALED && live) {
@@ -118,19 +138,15 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
             vr = rint(ldexp(vr, sh));
             vi = rint(ldexp(vi, sh));
         }
-        if (SPLIT3) {
-            x2r[e] = rint(vr * kTwoM52); vr = fma(-x2r[e], kTwo52, vr);
-            x2i[e] = rint(vi * kTwoM52); vi = fma(-x2i[e], kTwo52, vi);
-        }
-        x1r[e] = rint(vr * kTwoM26); x0r[e] = fma(-x1r[e], kTwo26, vr);
-        x1i[e] = rint(vi * kTwoM26); x0i[e] = fma(-x1i[e], kTwo26, vi);
+        split_digits<D>(vr, xr, e);
+        split_digits<D>(vi, xi, e);
     }
 
     // ---- residues and 2M pre per modulus (step 4, eq. 2m-pre) -------------
     int8_t *dst_p = planes + plane_offset(r, kk0 + kofs_p * kStageK, plane_kblocks);
     int8_t *dst_m = planes + plane_offset(r, kk0 + kofs_m * kStageK, plane_kblocks) + plane_bytes;
-    for (int l = 0; l < rp.n; ++l) {
-        const double c26 = rp.c26[l], c52 = rp.c52[l], inv = rp.inv[l];
+    for (int l = 0; l < rp.n2; ++l) {
+        const double inv = rp.inv[l];
         const double s = (double)rp.root[l];
         const uint32_t negm = (uint32_t)(-rp.mod[l]) & 0xFFFFFFu;
         uint32_t wp[4], wm[4];
@@ -140,9 +156,12 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int e = 4 * q + t;
-                double R = fma(c26, x1r[e], x0r[e]);
-                double I = fma(c26, x1i[e], x0i[e]);
-                if (SPLIT3) { R = fma(c52, x2r[e], R); I = fma(c52, x2i[e], I); }
+                double R = (double)xr[0][e], I = (double)xi[0][e];
+#pragma unroll
+                for (int d = 1; d < D; ++d) {
+                    R = fma(rp.cpow[l][d - 1], (double)xr[d][e], R);
+                    I = fma(rp.cpow[l][d - 1], (double)xi[d][e], I);
+                }
                 const double Ap = fma(s, I, R), Am = fma(-s, I, R);
                 const double tp = fma(Ap, inv, kMagic), tm = fma(Am, inv, kMagic);
                 const uint32_t ap = lo32(Ap + kMagic), am = lo32(Am + kMagic);
@@ -155,30 +174,71 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
         *reinterpret_cast<uint4 *>(dst_p + (size_t)(2 * l) * plane_bytes) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
         *reinterpret_cast<uint4 *>(dst_m + (size_t)(2 * l) * plane_bytes) = make_uint4(wm[0], wm[1], wm[2], wm[3]);
     }
+
+    // ---- hybrid sets: residues of Xr, Xi and Xr + Xi for 3M (Section 3.2) ---
+    for (int l = rp.n2; l < rp.n; ++l) {
+        const double inv = rp.inv[l];
+        const uint32_t negm = (uint32_t)(-rp.mod[l]) & 0xFFFFFFu;
+        uint32_t w[3][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t by[3][4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int e = 4 * q + t;
+                double R = (double)xr[0][e], I = (double)xi[0][e];
+#pragma unroll
+                for (int d = 1; d < D; ++d) {
+                    R = fma(rp.cpow[l][d - 1], (double)xr[d][e], R);
+                    I = fma(rp.cpow[l][d - 1], (double)xi[d][e], I);
+                }
+                const double v[3] = {R, I, R + I};
+#pragma unroll
+                for (int c = 0; c < 3; ++c) {
+                    const double tq = fma(v[c], inv, kMagic);
+                    by[c][t] = mad24(lo32(tq), negm, lo32(v[c] + kMagic));
+                }
+            }
+#pragma unroll
+            for (int c = 0; c < 3; ++c) w[c][q] = pack4(by[c][0], by[c][1], by[c][2], by[c][3]);
+        }
+        const size_t p0 = (size_t)(2 * rp.n2 + 3 * (l - rp.n2));
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+            *reinterpret_cast<uint4 *>(dst_p + (p0 + c) * plane_bytes) = make_uint4(w[c][0], w[c][1], w[c][2], w[c][3]);
+    }
 }
 
 }  // namespace
 
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
-                           bool wide, int khalf, const PlaneGeom &g, const ResidueParams &rp,
+                           int digits, int khalf, const PlaneGeom &g, const ResidueParams &rp,
                            int8_t *planes, hipStream_t st) {
     const int kreal = khalf > 0 ? g.kreal : 0;
     const long waves = (long)(g.rows_pad / kFragRows) * (long)g.kblocks;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
-    const bool split3 = wide;
-#define O2M_RES(M, T, S3, SC)                                                                    \
-    residue_kernel<M, T, S3, SC><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k,     \
+#define O2M_RES(M, T, DD, SC)                                                                    \
+    residue_kernel<M, T, DD, SC><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k,     \
                                                         g.rows_pad, g.kblocks, g.plane_kblocks,   \
                                                         g.kofs_p, g.kofs_m, g.plane_bytes, rp,    \
                                                         planes)
-    if (mode == 0 && et == kF64) { if (split3) O2M_RES(0, kF64, true, true); else O2M_RES(0, kF64, false, true); }
-    else if (mode == 1 && et == kF64) { if (split3) O2M_RES(1, kF64, true, true); else O2M_RES(1, kF64, false, true); }
-    else if (mode == 0 && et == kF32) { if (split3) O2M_RES(0, kF32, true, true); else O2M_RES(0, kF32, false, true); }
-    else if (mode == 1 && et == kF32) { if (split3) O2M_RES(1, kF32, true, true); else O2M_RES(1, kF32, false, true); }
-    else if (mode == 2 && et == kR64) { if (split3) O2M_RES(2, kR64, true, true); else O2M_RES(2, kR64, false, true); }
-    else if (mode == 0 && et == kI32) O2M_RES(0, kI32, false, false);
-    else if (mode == 1 && et == kI32) O2M_RES(1, kI32, false, false);
+#define O2M_RES_D(M, T)                                       \
+    switch (digits) {                                         \
+    case 2: O2M_RES(M, T, 2, true); break;                    \
+    case 3: O2M_RES(M, T, 3, true); break;                    \
+    case 4: O2M_RES(M, T, 4, true); break;                    \
+    case 5: O2M_RES(M, T, 5, true); break;                    \
+    default: return hipErrorInvalidValue;                     \
+    }
+    if (mode == 0 && et == kF64) { O2M_RES_D(0, kF64) }
+    else if (mode == 1 && et == kF64) { O2M_RES_D(1, kF64) }
+    else if (mode == 0 && et == kF32) { O2M_RES_D(0, kF32) }
+    else if (mode == 1 && et == kF32) { O2M_RES_D(1, kF32) }
+    else if (mode == 2 && et == kR64) { O2M_RES_D(2, kR64) }
+    else if (mode == 0 && et == kI32) O2M_RES(0, kI32, 2, false);
+    else if (mode == 1 && et == kI32) O2M_RES(1, kI32, 2, false);
     else return hipErrorInvalidValue;
+#undef O2M_RES_D
 #undef O2M_RES
     return hipGetLastError();
 }

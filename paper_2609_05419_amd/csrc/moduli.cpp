@@ -1,5 +1,6 @@
 // Host-side number theory for the 2M + Ozaki-II library: the 2M moduli
-// (Section 2 criterion, Section 4 greedy set), roots of -1, the scaling
+// (Section 2 criterion, Section 4 greedy set) and their hybrid 3M extension
+// (Section 3.2), roots of -1, the scaling
 // budget and the CRT weights folded with the 2M post step (eq. 2m-post),
 // stored as balanced base-2^40 limbs for the exact fp64 CRT of the CRT kernel.
 #include <math.h>
@@ -220,13 +221,31 @@ int moduli_2m(int *out, int cap) {
     return n;
 }
 
+int moduli_extension(int *out, int cap) {
+    // Section 3.2 (hybrid 2M / 3M): continue the greedy scan over all
+    // integers, coprime to the 2M set and to every extension modulus kept.
+    int kept[128];
+    int n = moduli_2m(kept, 64);
+    const int n2 = n;
+    for (int m = 256; m >= 2; --m) {
+        bool ok = true;
+        for (int i = 0; i < n; ++i)
+            if (gcd(m, kept[i]) != 1) { ok = false; break; }
+        if (ok && n < 128) kept[n++] = m;
+    }
+    for (int i = n2; i < n && i - n2 < cap; ++i) out[i - n2] = kept[i];
+    return n - n2;
+}
+
 const ModuliTable *moduli_table(int n) {
     if (n < 1 || n > kMaxModuli) return nullptr;
     std::lock_guard<std::mutex> lock(g_mu);
     if (g_tables[n]) return g_tables[n];
 
-    int all[64];
-    moduli_2m(all, 64);
+    int all[128];
+    const int n2all = moduli_2m(all, 64);
+    moduli_extension(all + n2all, 64);
+    const int n2 = n < n2all ? n : n2all;
     ModuliTable *t = new ModuliTable();
     memset(t, 0, sizeof *t);
     t->n = n;
@@ -240,21 +259,26 @@ const ModuliTable *moduli_table(int n) {
     // residue constants
     ResidueParams &rp = t->res;
     rp.n = n;
+    rp.n2 = n2;
     for (int l = 0; l < n; ++l) {
         int m = all[l];
         rp.mod[l] = m;
-        rp.root[l] = root_of_minus_one(m);
+        rp.root[l] = l < n2 ? root_of_minus_one(m) : 0;
         rp.inv[l] = 1.0 / (double)m;
-        int64_t p26 = 1, p52;
+        int64_t p26 = 1;
         for (int b = 0; b < 26; ++b) p26 = p26 * 2 % m;
-        p52 = p26 * p26 % m;
-        rp.c26[l] = (double)symmetric(p26, m);
-        rp.c52[l] = (double)symmetric(p52, m);
+        int64_t pw = 1;
+        for (int d = 1; d < kMaxDigits; ++d) {          // 2^(26 d) mod m
+            pw = pw * p26 % m;
+            rp.cpow[l][d - 1] = (double)symmetric(pw, m);
+        }
     }
 
-    // CRT weights folded with 2^-1 (Re) and s 2^-1 (Im), eq. 2m-post
+    // CRT weights folded with 2^-1 (Re) and s 2^-1 (Im), eq. 2m-post; plain
+    // weights for the 3M moduli of a hybrid set
     CrtParams &cp = t->crt;
     cp.n = n;
+    cp.n2 = n2;
     cp.limbs = (int)ceil((t->log2M + 1.0) / kLimbBits);
     if (cp.limbs < 2) cp.limbs = 2;
     for (int l = 0; l < n; ++l) {
@@ -264,6 +288,10 @@ const ModuliTable *moduli_table(int n) {
         uint32_t Ml_mod;
         big_div_small(Ml, (uint32_t)m, &Ml_mod);
         int inv_Ml = mod_inverse((int)Ml_mod, m);
+        if (l >= n2) {
+            balanced_limbs(Ml, symmetric(inv_Ml, m), cp.limbs, cp.wre[l]);
+            continue;
+        }
         int half = (m + 1) / 2;                             // 2^-1 mod m (Section 2)
         int s = rp.root[l];
         int gre = symmetric((int64_t)inv_Ml * half, m);

@@ -8,8 +8,11 @@
 
 namespace o2m {
 
-constexpr int kMaxModuli = 22;
-constexpr int kMaxLimbs = 4;
+constexpr int kMax2M = 22;        // the 2M moduli (Section 4)
+constexpr int kMaxModuli = 32;    // with up to 10 hybrid 3M moduli (Section 3.2)
+constexpr int kMaxProducts = 2 * kMax2M + 3 * (kMaxModuli - kMax2M);  // int8 GEMMs per call
+constexpr int kMaxLimbs = 6;
+constexpr int kMaxDigits = 5;     // base-2^26 digits of a quantized value (K2)
 constexpr int kLimbBits = 40;  // CRT limb base 2^40: limb sums stay below 2^53
 constexpr int kStatusOverflow = 1;  // device status bit: gauss-mode bound violated
 
@@ -51,26 +54,32 @@ inline int round_up(int x, int q) { return (x + q - 1) / q * q; }
 // ---------------------------------------------------------------------------
 
 // Residue step (eq. 2m-pre): per modulus m, its root s, fl(1/m) and the
-// symmetric residues of 2^26 and 2^52 used to reduce a quantized integer
-// x = x2 2^52 + x1 2^26 + x0 without integer division.
+// symmetric residues cpow[d-1] of 2^(26 d), d = 1..4, used to reduce a
+// quantized integer x = sum_d x_d 2^(26 d) without integer division.  Moduli 0..n2-1 are 2M
+// moduli (planes 2l = X+, 2l+1 = X-); moduli n2..n-1 are the 3M extension of a
+// hybrid set (planes 2 n2 + 3 (l - n2) + {0, 1, 2} = Xr, Xi, Xr + Xi).
 struct ResidueParams {
     int n;                       // number of moduli N
+    int n2;                      // of which 2M moduli
     int mod[kMaxModuli];
     int root[kMaxModuli];
     double inv[kMaxModuli];
-    double c26[kMaxModuli];
-    double c52[kMaxModuli];
+    double cpow[kMaxModuli][kMaxDigits - 1];
 };
 
 // CRT step (eq. 2m-post folded into Algorithm 1 step 5): X_re = sum_l u_l W^re_l,
 // X_im = sum_l v_l W^im_l with u = C- + C+, v = C- - C+ and
 // W^re_l = (M/m_l) * [((M/m_l)^-1 2^-1) mod m_l],
 // W^im_l = (M/m_l) * [((M/m_l)^-1 s_l 2^-1) mod m_l], as T balanced limbs.
+// For a 3M modulus of a hybrid set, u = T1 - T2, v = T3 - T1 - T2 (3M post)
+// and both parts use the plain weight W_l = (M/m_l) [(M/m_l)^-1 mod m_l],
+// stored in wre.
 struct CrtParams {
     int n;                        // N
+    int n2;                       // 2M moduli among them
     int limbs;                    // T
     double wre[kMaxModuli][kMaxLimbs];
-    double wim[kMaxModuli][kMaxLimbs];
+    double wim[kMax2M][kMaxLimbs];
     double mlimb[kMaxLimbs];      // M in balanced limbs
     double inv_m;                 // fl(1/M)
     uint64_t m_lo, m_hi;          // M (gauss mode: M < 2^63, m_hi = 0)
@@ -88,10 +97,14 @@ struct ModuliTable {
     int mwords_len;
 };
 
-// Returns the table for n moduli (1..kMaxModuli), building it on first use.
+// Returns the table for n moduli (1..kMaxModuli), building it on first use:
+// the first min(n, 22) 2M moduli, then n - 22 moduli of the 3M extension.
 const ModuliTable *moduli_table(int n);
 // The 2M moduli in greedy order (Section 4); returns the count (22).
 int moduli_2m(int *out, int cap);
+// The hybrid extension (Section 3.2): the greedy scan from 256 down over all
+// integers coprime to the 2M set and to each other; returns the count.
+int moduli_extension(int *out, int cap);
 // Smallest s with s^2 = -1 mod m, or 0 if none.
 int root_of_minus_one(int m);
 // Largest P with 2k 2^P <= (M-1)/2 - floor(M/2^32).
@@ -126,7 +139,8 @@ hipError_t launch_cs_exponents(int count, const unsigned long long *U, int32_t *
 //   mode 1: operand rows are columns of X (B, k x n), element (r, kk) at X[kk + r*ld]
 //   mode 2: SYRK, X real n x k, element (r, kk) = X[r + kk*ld] + i X[r + (kk+kh)*ld]
 //   shift: quantization shift p (value scaled by 2^(p - E_r)); E may be NULL (gauss).
-//   wide: some |quantized value| may exceed 2^62 (three-way split needed).
+//   digits: base-2^26 digits of the quantized values, from their bound
+//   (residue_digits).
 // Plane 2l receives X+ and plane 2l+1 receives X-; the source's k-block j
 // lands in k-block j + kofs_p of the + plane and j + kofs_m of the - plane
 // (rank-2k updates concatenate two sources along k; otherwise both are 0).
@@ -139,12 +153,19 @@ struct PlaneGeom {
     size_t plane_bytes;  // rows_pad * plane_kblocks * 64
 };
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
-                           bool wide, int khalf, const PlaneGeom &g, const ResidueParams &rp,
+                           int digits, int khalf, const PlaneGeom &g, const ResidueParams &rp,
                            int8_t *planes, hipStream_t st);
+// Digits for quantized values below 2^bits: 2 up to 62 bits, 3 up to 88
+// (top digit < 2^36), 4 up to 108 and 5 up to 134 (top digit < 2^30, int32);
+// 0 if more are needed.
+inline int residue_digits(int bits) {
+    return bits <= 62 ? 2 : bits <= 88 ? 3 : bits <= 108 ? 4 : bits <= 134 ? 5 : 0;
+}
 
 // K3: batched int8 GEMM  C_p = A_p B_p^T  (both operands K-major planes), then
-// C_p mod m_(p >> mod_shift) stored as int8 (symmetric residue), column-major
-// with leading dimension ldc = m_pad, plane stride ldc * n_pad.
+// C_p mod m_p stored as int8 (symmetric residue), column-major with leading
+// dimension ldc = m_pad, plane stride ldc * n_pad.  mod[p], inv[p]: the
+// modulus of product p and its fp64 reciprocal.
 struct GemmArgs {
     const int8_t *a;
     const int8_t *b;
@@ -152,11 +173,10 @@ struct GemmArgs {
     size_t a_pstride, b_pstride, c_pstride;  // bytes between consecutive batch items
     int mt, nt, kblocks;                     // tiles along m, n; k stages
     int batch;
-    int mod_shift;
     int ldc;
     int chunk;                               // tiles per XCD per product (set by the launcher)
-    int mod[kMaxModuli];
-    double inv[kMaxModuli];
+    int mod[kMaxProducts];
+    double inv[kMaxProducts];
 };
 hipError_t launch_gemm(const GemmArgs &ga, hipStream_t st);
 
@@ -178,8 +198,10 @@ struct CrtArgs {
     const unsigned long long *amaxA, *amaxB;  // gauss mode bound check
     int k;
     int *status;
-    ResidueParams rp;   // hook mode
+    short hmod[kMaxModuli], hroot[kMaxModuli];  // hook mode: moduli and roots
 };
+// Both go to the CRT kernels by value: stay within the kernel-argument limit.
+static_assert(sizeof(CrtArgs) + sizeof(CrtParams) <= 4000, "CRT kernel arguments");
 hipError_t launch_crt(int mode, ElemType out_type, const CrtArgs &ca, const CrtParams &cp,
                       hipStream_t st);
 

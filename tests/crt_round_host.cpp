@@ -2,17 +2,34 @@
 #define O2M_HD
 #include "../paper_2609_05419_amd/csrc/crt_round.h"
 
+namespace {
+template <int T>
+double lift(const double *S, const double *mlimb, double inv_m, int sc) {
+    double s[T];
+    for (int t = 0; t < T; ++t) s[t] = S[t];
+    return o2m::lift_round<T>(s, mlimb, inv_m, sc);
+}
+}  // namespace
+
 extern "C" {
 double t_sum3_rn(double a, double b, double c) { return o2m::sum3_rn(a, b, c); }
 double t_round_limbs(const int64_t *limbs, int T, int sc) {
-    o2m::U192 v = {0, 0, 0};
-    for (int t = 0; t < T; ++t) o2m::add_shifted(v, limbs[t], 40 * t);
-    return o2m::round_u192(v, sc);
+    if (T <= 4) {
+        o2m::UW<3> v = {};
+        for (int t = 0; t < T; ++t) o2m::add_shifted<3>(v, limbs[t], 40 * t);
+        return o2m::round_words<3>(v, sc);
+    }
+    o2m::UW<4> v = {};
+    for (int t = 0; t < T; ++t) o2m::add_shifted<4>(v, limbs[t], 40 * t);
+    return o2m::round_words<4>(v, sc);
 }
 double t_lift_round(const double *S, int T, const double *mlimb, double inv_m, int sc) {
-    if (T == 2) { const double s[2] = {S[0], S[1]}; return o2m::lift_round<2>(s, mlimb, inv_m, sc); }
-    if (T == 3) { const double s[3] = {S[0], S[1], S[2]}; return o2m::lift_round<3>(s, mlimb, inv_m, sc); }
-    const double s[4] = {S[0], S[1], S[2], S[3]};
-    return o2m::lift_round<4>(s, mlimb, inv_m, sc);
+    switch (T) {
+    case 2: return lift<2>(S, mlimb, inv_m, sc);
+    case 3: return lift<3>(S, mlimb, inv_m, sc);
+    case 4: return lift<4>(S, mlimb, inv_m, sc);
+    case 5: return lift<5>(S, mlimb, inv_m, sc);
+    default: return lift<6>(S, mlimb, inv_m, sc);
+    }
 }
 }

@@ -48,18 +48,20 @@ def test_package_binding_loads():
 
 def test_moduli_table_matches_oracle():
     import paper_2609_05419_amd as o2m
-    for n in (1, 4, 8, 16, 22):
+    for n in (1, 4, 8, 16, 22, 23, 27, 32):
         ms, ss, l2 = o2m.moduli(n)
-        assert ms == O.moduli_2m(n)
-        assert ss == [O.root_of(q) for q in ms]
+        assert ms == O.moduli_set(n)
+        assert ss == [O.root_of(q) if O.is_2m_modulus(q) else 0 for q in ms]
         assert abs(l2 - __import__("math").log2(O.product(ms))) < 1e-9
+    with pytest.raises(o2m.O2MError):
+        o2m.moduli(33)
 
 
 def test_budget_matches_oracle():
     import paper_2609_05419_amd as o2m
-    for n in (1, 2, 3, 4, 5, 8, 12, 16, 17, 20, 22):
-        for k in (0, 1, 2, 7, 64, 1000, 1024, 8192, 16384, 65536, 149130):
-            assert o2m.budget(n, k) == O.budget(O.moduli_2m(n), k), (n, k)
+    for n in (1, 2, 3, 4, 5, 8, 12, 16, 17, 20, 22, 23, 26, 29, 32):
+        for k in (0, 1, 2, 7, 64, 1000, 1024, 8192, 16384, 65536, 131071, 149130):
+            assert o2m.budget(n, k) == O.budget(O.moduli_set(n), k), (n, k)
 
 
 def test_workspace_bytes_grow_with_the_problem():
@@ -72,7 +74,11 @@ def test_workspace_bytes_grow_with_the_problem():
     assert h < z
     s = o2m.workspace_bytes("s", 8192, 8192, 8192, 16)
     assert s < h
-    assert o2m.workspace_bytes("z", 8192, 8192, 8192, 23) == 0
+    assert o2m.workspace_bytes("z", 8192, 8192, 8192, 33) == 0
+    assert o2m.workspace_bytes("h", 8192, 8192, 8192, 23) == 0
+    # hybrid: 2 planes per 2M modulus and 3 per 3M modulus, on each side
+    z24 = o2m.workspace_bytes("z", 8192, 8192, 8192, 24)
+    assert z24 >= (2 * 22 + 3 * 2) * (8192 * 8192 * 3)
 
 
 def test_argument_errors_are_reported_before_any_gpu_work(lib):
@@ -90,8 +96,9 @@ def test_argument_errors_are_reported_before_any_gpu_work(lib):
     assert call(4, 4, 4, fake, 4, fake, 4, None, 4, 16, None) == -8
     assert call(4, 4, 4, fake, 4, fake, 4, fake, 3, 16, None) == -9
     assert call(4, 4, 4, fake, 4, fake, 4, fake, 4, 0, None) == -20
-    assert call(4, 4, 4, fake, 4, fake, 4, fake, 4, 23, None) == -20
+    assert call(4, 4, 4, fake, 4, fake, 4, fake, 4, 33, None) == -20
     assert call(4, 4, 149131, fake, 4, fake, 149131, fake, 4, 16, None) == -21
+    assert call(4, 4, 131072, fake, 4, fake, 131072, fake, 4, 23, None) == -21   # hybrid k limit
     # empty outputs are a no-op that touches nothing
     assert call(0, 4, 4, None, 1, fake, 4, fake, 1, 16, None) == 0
     assert call(4, 0, 4, fake, 4, fake, 4, None, 4, 16, None) == 0
@@ -99,6 +106,7 @@ def test_argument_errors_are_reported_before_any_gpu_work(lib):
     assert lib.gauss_gemm_2m(4, 4, 4, fake, 4, fake, 4, fake, 4, 9, None) == -20
     lib.zherk_2m.argtypes = [ctypes.c_char, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int, P]
     assert lib.zherk_2m(b"U", 4, 4, fake, 4, fake, 4, 16, None) == -1
+    assert lib.zherk_2m(b"L", 4, 4, fake, 4, fake, 4, 23, None) == -20    # symmetric calls: 2M only
     assert lib.zherk_2m(b"L", 4, 4, fake, 3, fake, 4, 16, None) == -5
     assert lib.zherk_2m(b"L", 0, 4, None, 1, None, 1, 16, None) == 0
     lib.o2m_status_string.restype = ctypes.c_char_p
@@ -115,12 +123,17 @@ def test_new_entry_points_declared():
 @pytest.mark.parametrize("scaling", ["max", "cs"])
 def test_shifts_match_oracle(scaling):
     import paper_2609_05419_amd as o2m
-    for n in (1, 2, 3, 4, 8, 12, 16, 17, 20, 22):
-        ms = O.moduli_2m(n)
+    for n in (1, 2, 3, 4, 8, 12, 16, 17, 20, 22, 23, 28, 32):
+        ms = O.moduli_set(n)
         for k in (0, 1, 2, 7, 64, 1000, 8192, 16384, 65536, 74565, 149130):
             cases = {"z": (k, False), "c": (k, False), "r": (k, False), "h": (k, True),
                      "s": ((k + 1) // 2, True), "x": (2 * k, True), "y": (2 * ((k + 1) // 2), True)}
             for op, (kin, sym) in cases.items():
+                if sym and n > 22:
+                    with pytest.raises(o2m.O2MError) as e:
+                        o2m.shifts(op, n, k, scaling)
+                    assert e.value.status == -20
+                    continue
                 try:
                     want = O.shifts(scaling, ms, kin, sym)
                 except ValueError:

@@ -1,6 +1,7 @@
 """Host build of the CRT kernel's rounding (crt_round.h) against Python's
 correctly rounded int -> float conversion: the three-term round-to-odd sum, the
-192-bit path, and the full lift with real CRT tables built by the oracle."""
+multiword paths (192 and 256 bits), and the full lift with real CRT tables
+built by the oracle (2M and hybrid sets)."""
 import ctypes
 import math
 import os
@@ -70,23 +71,25 @@ def test_three_term_sum_is_correctly_rounded(lib):
         assert got == float(c), c
 
 
-def test_192_bit_rounding(lib):
-    rng = random.Random(4)
-    for c in interesting_integers(rng, 150):
-        limbs = split_limbs(c, 4, rng)
+@pytest.mark.parametrize("T,bits", [(4, 150), (5, 190), (6, 245)])
+def test_multiword_rounding(lib, T, bits):
+    rng = random.Random(T)
+    for c in interesting_integers(rng, bits):
+        limbs = split_limbs(c, T, rng)
         arr = np.array(limbs, dtype=np.int64)
-        for sc in (0, -1074 + 10, 200):
-            got = lib.t_round_limbs(arr.ctypes.data, 4, sc)
+        for sc in (0, -1074 + 10, 200, -500):
+            got = lib.t_round_limbs(arr.ctypes.data, T, sc)
             assert got == math.ldexp(float(c), sc) if c else got == 0.0, (c, sc)
 
 
-@pytest.mark.parametrize("N", [4, 8, 12, 16, 17, 22])
+@pytest.mark.parametrize("N", [4, 8, 12, 16, 17, 22, 23, 27, 28, 32])
 def test_lift_round_with_crt_tables(lib, N):
     """Limb sums built the way the CRT kernel builds them (balanced base-2^40
-    weights folded with 2^-1), lifted and rounded, equal RN of the exact
-    symmetric lift computed with Python integers."""
+    weights folded with 2^-1; plain weights for the 3M moduli of a hybrid set),
+    lifted and rounded, equal RN of the exact symmetric lift computed with
+    Python integers."""
     rng = random.Random(N)
-    ms = O.moduli_2m(N)
+    ms = O.moduli_set(N)
     M = O.product(ms)
     T = max(2, math.ceil((math.log2(M) + 1) / 40))
 
@@ -104,7 +107,8 @@ def test_lift_round_with_crt_tables(lib, N):
     W = []
     for q in ms:
         Ml = M // q
-        g = (pow(Ml % q, -1, q) * O.inv2(q)) % q
+        fold = O.inv2(q) if O.is_2m_modulus(q) else 1
+        g = (pow(Ml % q, -1, q) * fold) % q
         g = g - q if g > (q - 1) // 2 else g
         W.append(Ml * g)
     wl = [limbs(w) for w in W]
@@ -117,14 +121,21 @@ def test_lift_round_with_crt_tables(lib, N):
         # residues of c mod each m, split as u = r- + r+ with symmetric parts
         u = []
         for q in ms:
-            r = (c * 2) % q          # u = 2c mod q, since W folds in 2^-1
-            r = r - q if r > (q - 1) // 2 else r
-            rm = rng.randint(-(q - 1) // 2, (q - 1) // 2)
-            rp = r - rm
-            if abs(rp) > (q - 1) // 2:
-                rp = r
-                rm = 0
-            u.append(rm + rp)
+            if O.is_2m_modulus(q):
+                r = (c * 2) % q          # u = 2c mod q, since W folds in 2^-1
+                r = r - q if r > (q - 1) // 2 else r
+                rm = rng.randint(-(q - 1) // 2, (q - 1) // 2)
+                rp = r - rm
+                if abs(rp) > (q - 1) // 2:
+                    rp = r
+                    rm = 0
+                u.append(rm + rp)
+            else:                        # 3M: u = T1 - T2 with int8 residues
+                r = c % q
+                t2 = rng.randint(-(q // 2), (q - 1) // 2)
+                t1 = (r + t2) % q
+                t1 = t1 - q if t1 > (q - 1) // 2 else t1
+                u.append(t1 - t2)
         S = np.array([sum(u[l] * wl[l][t] for l in range(N)) for t in range(T)], dtype=np.float64)
         assert all(abs(sum(u[l] * wl[l][t] for l in range(N))) < 1 << 53 for t in range(T))
         sc = rng.randint(-60, 60)
