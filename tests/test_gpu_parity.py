@@ -386,3 +386,58 @@ def test_dsyrk_4096_sampled(o2m):
     ent = _sample(np.random.default_rng(13), n, n, 48, lower=True)
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_dsyrk(a, 16, entries=ent))
+
+
+# ------------------------------------------------------------------ layouts and streams
+
+
+def _padded_view(x, pad_rows):
+    """Device view of host matrix x inside a larger column-major buffer
+    (leading dimension rows + pad_rows), the padding filled with NaN so that a
+    read outside the view would poison the result."""
+    rows, cols = x.shape
+    big = np.full((rows + pad_rows, cols), np.nan, dtype=x.dtype)
+    big[:rows, :] = x
+    return to_dev(big)[:rows, :]
+
+
+def test_zgemm_strided_operands_and_output(o2m):
+    m, n, k = 70, 50, 90
+    a = W.complex_matrix(m, k, 401)
+    b = W.complex_matrix(k, n, 402)
+    A, B = _padded_view(a, 13), _padded_view(b, 7)
+    assert A.stride(1) == m + 13 and B.stride(1) == k + 7
+    Cbig = o2m.colmajor(torch.full((m + 5, n), 9.0 + 9j, dtype=torch.complex128, device=DEV))
+    C = Cbig[:m, :]
+    o2m.zgemm_2m(A, B, n_moduli=16, out=C)
+    got = host(Cbig)
+    assert same_bits(np.asfortranarray(got[:m, :]), O.oq_zgemm(a, b, 16))
+    assert (got[m:, :] == 9.0 + 9j).all()           # rows beyond m untouched
+
+
+def test_cgemm_and_zherk_strided(o2m):
+    a = W.complex_matrix(40, 33, 411, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(33, 21, 412, dist="uniform", dtype=np.complex64)
+    got = host(o2m.cgemm_2m(_padded_view(a, 3), _padded_view(b, 11), n_moduli=8))
+    assert same_bits(got, O.oq_cgemm(a, b, 8))
+    h = W.complex_matrix(45, 60, 413)
+    Cbig = o2m.colmajor(torch.zeros((45 + 6, 45), dtype=torch.complex128, device=DEV))
+    o2m.zherk_2m(_padded_view(h, 9), n_moduli=16, out=Cbig[:45, :])
+    got = host(Cbig)[:45, :]
+    ref = O.oq_zherk(h, 16)
+    low = np.tril(np.ones((45, 45), dtype=bool))
+    assert same_bits(got[low], ref[low])
+
+
+def test_calls_on_a_side_stream(o2m):
+    a = W.complex_matrix(120, 100, 421)
+    b = W.complex_matrix(100, 80, 422)
+    A, B = to_dev(a), to_dev(b)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        C1 = o2m.zgemm_2m(A, B, n_moduli=16)                 # current stream = s
+        C2 = o2m.zgemm_2m(A, B, n_moduli=12, stream=s)
+    s.synchronize()
+    assert same_bits(np.asfortranarray(C1.cpu().numpy()), O.oq_zgemm(a, b, 16))
+    assert same_bits(np.asfortranarray(C2.cpu().numpy()), O.oq_zgemm(a, b, 12))
