@@ -75,6 +75,56 @@ def cpu_baseline(a, b, n_moduli, rows, cols):
                       f"k={k}, {dt:.2f} s"}
 
 
+def error_curve() -> int:
+    """Error against the unquantized product over the whole output (the
+    accuracy-per-modulus curves): max |c~ - c| / (4 u k (|A||B|)_ij) (the
+    tolerance holds when <= 1), max |c~ - c| / |c| and the componentwise
+    maxima, for ZGEMM (1024^3, parts N(0,1)) at N = 6..22 and CGEMM (1024^3,
+    parts U(-1,1)) at N = 4..10, under both scaling rules."""
+    import torch
+
+    import oracle
+    import paper_2609_05419_amd as o2m
+    import workloads
+
+    dev = torch.device("cuda:0")
+
+    def to_dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x.T)).to(dev).t()
+
+    m = n = k = 1024
+    sa, sb = workloads.config_seeds(2)
+    for op, dist, dtype, u, Ns in (("zgemm", "normal", np.complex128, 2.0 ** -53, range(6, 23, 2)),
+                                   ("cgemm", "uniform", np.complex64, 2.0 ** -24, range(4, 11))):
+        a = workloads.complex_matrix(m, k, sa, dist=dist, dtype=dtype)
+        b = workloads.complex_matrix(k, n, sb, dist=dist, dtype=dtype)
+        a64, b64 = a.astype(np.complex128), b.astype(np.complex128)
+        t0 = time.perf_counter()
+        hi, lo = oracle.dd_gemm(a64, b64)
+        absab = np.abs(a64) @ np.abs(b64)
+        log(f"bench: dd reference {op} in {time.perf_counter() - t0:.1f} s")
+        A, B = to_dev(a), to_dev(b)
+        native = (torch.matmul(A, B)).cpu().numpy().astype(np.complex128)
+        nerr = oracle.error_vs_reference(native, absab, hi, lo, k, u)
+        print(json.dumps({"report": "error_curve", "op": op, "n_moduli": None, "scaling_rule": "native torch.matmul",
+                          **{kk: nerr[kk] for kk in ("ratio", "maxrel", "maxrel_re", "maxrel_im", "zeros")}}), flush=True)
+        fn = o2m.zgemm_2m if op == "zgemm" else o2m.cgemm_2m
+        for rule in ("max", "cs"):
+            for N in Ns:
+                try:
+                    C = fn(A, B, n_moduli=N, scaling=rule)
+                except o2m.O2MError as e:
+                    log(f"bench: {op} N={N} {rule}: {e}")
+                    continue
+                got = C.cpu().numpy().astype(np.complex128)
+                err = oracle.error_vs_reference(got, absab, hi, lo, k, u)
+                print(json.dumps({"report": "error_curve", "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
+                                  "scaling_rule": rule,
+                                  **{kk: err[kk] for kk in ("ratio", "maxrel", "maxrel_re", "maxrel_im", "zeros")}}),
+                      flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -84,6 +134,10 @@ def main() -> int:
     ap.add_argument("--sweep-n", default="",
                     help="comma-separated moduli counts: one JSON line per N on the same inputs "
                          "(perf-vs-precision sweep; not the default single-line run)")
+    ap.add_argument("--error-curve", action="store_true",
+                    help="accuracy report instead of timing: ZGEMM 1024^3 N(0,1) and CGEMM 1024^3 "
+                         "U(-1,1), every entry against the double-double oracle, for each moduli "
+                         "count and scaling rule; one JSON line per point")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--m", type=int, default=8192)
@@ -108,6 +162,9 @@ def main() -> int:
         torch.cuda.synchronize()
         log(f"bench: copied {n} bytes twice")
         return 0
+
+    if args.error_curve:
+        return error_curve()
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
