@@ -75,6 +75,33 @@ def cpu_baseline(a, b, n_moduli, rows, cols):
                       f"k={k}, {dt:.2f} s"}
 
 
+def hbm_probe(torch) -> dict:
+    """STREAM-like rates of plain torch kernels on 4 GiB (after the timed
+    region): device copy (read + write), sum (read), fill (write)."""
+    n = 4 << 30
+    out = {}
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    x = src.view(torch.float64)
+    tests = (("copy_GBs", lambda: dst.copy_(src), 2 * n), ("read_GBs", lambda: x.sum(), n),
+             ("write_GBs", lambda: dst.fill_(3), n))
+    for name, fn, nbytes in tests:
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(5):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        out[name] = round(nbytes / (s.elapsed_time(e) / 5 * 1e-3) / 1e9, 1)
+    del src, dst, x
+    torch.cuda.empty_cache()
+    return out
+
+
 def error_curve() -> int:
     """Error against the unquantized product over the whole output (the
     accuracy-per-modulus curves): max |c~ - c| / (4 u k (|A||B|)_ij) (the
@@ -347,6 +374,9 @@ def main() -> int:
                 del Cn
             except Exception as e:
                 log(f"bench: native comparison skipped: {e}")
+
+        if with_extras:
+            hbm["practical"] = hbm_probe(torch)
 
         cpu = None
         if with_extras and not args.no_cpu_baseline and op == "zgemm" and rule == "max":

@@ -441,3 +441,17 @@ def test_calls_on_a_side_stream(o2m):
     s.synchronize()
     assert same_bits(np.asfortranarray(C1.cpu().numpy()), O.oq_zgemm(a, b, 16))
     assert same_bits(np.asfortranarray(C2.cpu().numpy()), O.oq_zgemm(a, b, 12))
+
+
+@pytest.mark.slow
+def test_zgemm_k_at_the_int32_limit_sampled(o2m):
+    """k = 149130, the largest k whose int32 accumulation is exact with 2M
+    residues (|r| <= 120): the longest k-loop of the plain calls."""
+    m, n, k = 256, 300, 149130
+    a = W.complex_matrix(m, k, 431)
+    b = W.complex_matrix(k, n, 432)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    rng = np.random.default_rng(26)
+    ent = [(0, 0), (m - 1, n - 1)] + [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 30), rng.integers(0, n, 30))]
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))

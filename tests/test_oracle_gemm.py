@@ -248,3 +248,26 @@ def test_error_shrinks_with_moduli_count_and_meets_tolerance():
         assert 2.0 < bits < 6.0, (N, bits)
     assert errs[16]["ratio"] <= 1.0
     assert errs[8]["ratio"] > 1.0
+
+
+def test_error_vs_reference_closed_form():
+    # c - ref = (3, 4) 2^-40 exactly (a 3-4-5 triangle: modulus 5 2^-40);
+    # |ref| = 5, |A||B| = 2, k = 8
+    d = 2.0 ** -40
+    ref_hi = np.array([3.0 + 4.0j, 0.0 + 0.0j, -6.0 + 8.0j])
+    ref_lo = np.zeros(3, dtype=complex)
+    c = ref_hi + np.array([3 * d + 4j * d, 0.0, 0.0])
+    absab = np.array([2.0, 1.0, 1.0])
+    u = 2.0 ** -53
+    e = O.error_vs_reference(c, absab, ref_hi, ref_lo, 8, u)
+    assert math.isclose(e["maxrel"], 5 * d / 5.0, rel_tol=1e-12)
+    assert math.isclose(e["ratio"], 5 * d / (4 * u * 8 * 2.0), rel_tol=1e-12)
+    assert math.isclose(e["maxrel_re"], 3 * d / 3.0, rel_tol=1e-12)
+    assert math.isclose(e["maxrel_im"], 4 * d / 4.0, rel_tol=1e-12)
+    assert e["zeros"] == 1
+    # the low word of the reference counts: an error hidden in ref_lo is seen
+    e2 = O.error_vs_reference(ref_hi, absab, ref_hi, np.array([1e-20, 0, 0], dtype=complex), 8, u)
+    assert math.isclose(e2["maxrel"], 1e-20 / 5.0, rel_tol=1e-12)
+    # an error where |A||B| is zero is an infinite ratio
+    e3 = O.error_vs_reference(np.array([1e-300 + 0j]), np.array([0.0]), np.array([0j]), np.array([0j]), 8, u)
+    assert e3["ratio"] == math.inf
