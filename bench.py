@@ -102,6 +102,26 @@ def hbm_probe(torch) -> dict:
     return out
 
 
+def mfma_ceiling(torch) -> dict:
+    """The int8 MFMA rate the chip sustains on register operands (no memory
+    traffic), from the probe library: the practical ceiling of the int8 GEMM
+    under the part's power budget (random operands), next to zero operands
+    and the 32x32x32 instruction."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2609_05419_amd", "libo2m_probe.so")
+    L = ctypes.CDLL(path)
+    L.o2m_probe_int8_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    L.o2m_probe_int8_mfma.restype = ctypes.c_double
+    blocks, iters = 2048, 512
+    out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    res = {}
+    for name, variant in (("mfma16x16x64_random_TOPS", 0), ("mfma16x16x64_zero_TOPS", 1),
+                          ("mfma32x32x32_random_TOPS", 2)):
+        res[name] = round(L.o2m_probe_int8_mfma(variant, blocks, iters, out.data_ptr(), st), 1)
+    return res
+
+
 def error_curve() -> int:
     """Error against the unquantized product over the whole output (the
     accuracy-per-modulus curves): max |c~ - c| / (4 u k (|A||B|)_ij) (the
@@ -375,8 +395,14 @@ def main() -> int:
             except Exception as e:
                 log(f"bench: native comparison skipped: {e}")
 
+        ceiling = None
         if with_extras:
             hbm["practical"] = hbm_probe(torch)
+            try:
+                ceiling = mfma_ceiling(torch)
+                ceiling["gemm_frac_of_random_ceiling"] = round(achieved / ceiling["mfma16x16x64_random_TOPS"], 4)
+            except OSError as e:
+                log(f"bench: MFMA probe skipped: {e}")
 
         cpu = None
         if with_extras and not args.no_cpu_baseline and op == "zgemm" and rule == "max":
@@ -400,6 +426,7 @@ def main() -> int:
                        "phi": args.phi if op == "zgemm" else None, "scaling_rule": rule,
                        "parallelism": "single GPU"},
             "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
+            "int8_mfma_ceiling": ceiling,
             "phase_ms": {kk: round(v, 4) for kk, v in phases.items()},
             "hbm": hbm,
             "roofline": roofline,

@@ -10,6 +10,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libo2m.so")
 SOURCES = ["api.hip", "k_scale.hip", "k_residue.hip", "k_gemm.hip", "k_crt.hip", "moduli.cpp"]
+# measurement probe (the practical int8 MFMA ceiling), a library of its own
+PROBE_LIB = os.path.join(HERE, "libo2m_probe.so")
+PROBE_SOURCES = ["probe_mfma.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -21,7 +24,12 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    _build_one(PROBE_LIB, PROBE_SOURCES, verbose)
+    return _build_one(LIB, SOURCES, verbose)
+
+
+def _build_one(LIB: str, sources, verbose: bool) -> str:
+    srcs = [os.path.join(CSRC, s) for s in sources]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-o", tmp, *srcs]
     if verbose:
@@ -30,7 +38,7 @@ def build(verbose: bool = False) -> str:
     lines = [l for l in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in l]
     if r.returncode != 0:
         sys.stderr.write("\n".join(lines) + "\n")
-        raise RuntimeError("hipcc failed building libo2m.so")
+        raise RuntimeError(f"hipcc failed building {os.path.basename(LIB)}")
     if verbose and lines:
         print("\n".join(lines))
     os.replace(tmp, LIB)
