@@ -170,3 +170,21 @@ def test_rank2k_and_scaling_argument_errors(lib):
     assert lib.zgemm_2m_ex(4, 4, 8192, fake, 4, fake, 8192, fake, 4, 1, 1, None) == -26  # no CS shifts
     lib.o2m_status_string.restype = ctypes.c_char_p
     assert b"scaling" in lib.o2m_status_string(-26)
+
+
+def test_probe_library_exports_its_header():
+    path = os.path.join(ROOT, "paper_2609_05419_amd", "libo2m_probe.so")
+    if not os.path.exists(path):
+        pytest.skip("libo2m_probe.so not built")
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "o2m_probe.h")).read(), flags=re.S)
+    names = re.findall(r"^\s*(?:double|int|void)\s*(\w+)\s*\(", text, flags=re.M)
+    assert names == ["o2m_probe_int8_mfma"]
+    L = ctypes.CDLL(path)
+    for n in names:
+        assert hasattr(L, n)
+    L.o2m_probe_int8_mfma.restype = ctypes.c_double
+    L.o2m_probe_int8_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    # bad arguments are refused before any GPU call
+    assert L.o2m_probe_int8_mfma(3, 1, 1, ctypes.c_void_p(0x1000), None) < 0
+    assert L.o2m_probe_int8_mfma(0, 0, 1, ctypes.c_void_p(0x1000), None) < 0
+    assert L.o2m_probe_int8_mfma(0, 1, 1, None, None) < 0
