@@ -152,3 +152,52 @@ def test_zgemm_8192_hybrid_sampled(o2m):
     ent += [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 28), rng.integers(0, n, 28))]
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_zgemm(a, b, 26, entries=ent))
+
+
+@pytest.mark.slow
+def test_randomized_configurations(o2m):
+    """Seeded random combinations of call, shape, moduli count, scaling rule and
+    input distribution, each bit-exact against the oracle (a sweep over the
+    corners the fixed cases do not combine)."""
+    rng = np.random.default_rng(2609)
+    ops = ["zgemm", "cgemm", "zherk", "dsyrk", "zher2k", "dsyr2k"]
+    low = lambda n: np.tril(np.ones((n, n), dtype=bool))
+    for case in range(36):
+        op = ops[case % len(ops)]
+        sym = op not in ("zgemm", "cgemm")
+        N = int(rng.integers(1, 23 if sym else 33))
+        rule = "cs" if rng.random() < 0.5 else "max"
+        m, n, k = (int(x) for x in rng.integers(1, 300, 3))
+        k = max(1, k)
+        if rule == "cs" and O.budget_cs(O.moduli_set(N), 2 * k if op in ("zher2k", "dsyr2k") else k, sym) is None:
+            rule = "max"
+        dist = ["normal", "uniform", "phi"][int(rng.integers(0, 3))]
+        phi = float(rng.choice([0.5, 2.0, 4.0]))
+        seed = 9000 + case
+        print(f"[hybrid] random case {case}: {op} m={m} n={n} k={k} N={N} {rule} {dist}", flush=True)
+        if op in ("zgemm", "cgemm"):
+            dt = np.complex128 if op == "zgemm" else np.complex64
+            a = W.complex_matrix(m, k, seed, dist=dist, phi=phi, dtype=dt)
+            b = W.complex_matrix(k, n, seed + 1, dist=dist, phi=phi, dtype=dt)
+            fn = o2m.zgemm_2m if op == "zgemm" else o2m.cgemm_2m
+            ofn = O.oq_zgemm if op == "zgemm" else O.oq_cgemm
+            got = host(fn(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+            assert same_bits(got, ofn(a, b, N, scaling=rule)), case
+        elif op in ("zherk", "zher2k"):
+            a = W.complex_matrix(m, k, seed, dist=dist, phi=phi)
+            if op == "zherk":
+                got, ref = host(o2m.zherk_2m(to_dev(a), n_moduli=N, scaling=rule)), O.oq_zherk(a, N, scaling=rule)
+            else:
+                b = W.complex_matrix(m, k, seed + 1, dist=dist, phi=phi)
+                got = host(o2m.zher2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+                ref = O.oq_zher2k(a, b, N, scaling=rule)
+            assert same_bits(got[low(m)], ref[low(m)]), case
+        else:
+            a = W.real_matrix(m, k, seed, dist=dist, phi=phi)
+            if op == "dsyrk":
+                got, ref = host(o2m.dsyrk_2m(to_dev(a), n_moduli=N, scaling=rule)), O.oq_dsyrk(a, N, scaling=rule)
+            else:
+                b = W.real_matrix(m, k, seed + 1, dist=dist, phi=phi)
+                got = host(o2m.dsyr2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+                ref = O.oq_dsyr2k(a, b, N, scaling=rule)
+            assert same_bits(got[low(m)], ref[low(m)]), case
