@@ -101,6 +101,8 @@ struct Buffers {
 size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
     Carver c(base);
     Buffers t;
+    // amax_a, amax_b, ssq_a, ssq_b stay contiguous and in this order, ending
+    // where E begins: K1 clears them with one fill
     t.amax_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
     t.amax_b = g.shared_planes ? t.amax_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
     t.ssq_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
@@ -242,27 +244,19 @@ o2m_status run(const Call &c) {
 
     phase_mark(0, c.st);
     // ---- K1: maxima and exponents (rank-2k: row i of A and of B share one) --
-    O2M_TRY(launch_zero(b.amax_a, sizeof(unsigned long long) * g.a_pad, c.st));
+    // maxima and sums of squares start at zero: one fill over the contiguous
+    // amax_a .. ssq_b region of the workspace (carve order)
+    O2M_TRY(launch_zero(b.amax_a, (size_t)((char *)b.E - (char *)b.amax_a), c.st));
     O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
     if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
-    if (!sym) {
-        O2M_TRY(launch_zero(b.amax_b, sizeof(unsigned long long) * g.b_pad, c.st));
-        O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
-    }
-    if (c.op != kOpG) {
-        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, c.st));
-        if (!sym) O2M_TRY(launch_exponents(c.n, b.amax_b, b.F, c.st));
-    }
+    if (!sym) O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
+    if (c.op != kOpG)
+        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, c.st));
     if (cs) {
-        O2M_TRY(launch_zero(b.ssq_a, sizeof(unsigned long long) * g.a_pad, c.st));
         O2M_TRY(launch_ssq(0, et, c.m, c.k, c.A, c.lda, b.E, b.ssq_a, c.st));
         if (two) O2M_TRY(launch_ssq(0, et, c.m, c.k, c.B, c.ldb, b.E, b.ssq_a, c.st));
-        O2M_TRY(launch_cs_exponents(c.m, b.ssq_a, b.E, c.st));
-        if (!sym) {
-            O2M_TRY(launch_zero(b.ssq_b, sizeof(unsigned long long) * g.b_pad, c.st));
-            O2M_TRY(launch_ssq(1, et, c.k, c.n, c.B, c.ldb, b.F, b.ssq_b, c.st));
-            O2M_TRY(launch_cs_exponents(c.n, b.ssq_b, b.F, c.st));
-        }
+        if (!sym) O2M_TRY(launch_ssq(1, et, c.k, c.n, c.B, c.ldb, b.F, b.ssq_b, c.st));
+        O2M_TRY(launch_cs_exponents(c.m, b.ssq_a, b.E, sym ? 0 : c.n, b.ssq_b, b.F, c.st));
     }
     phase_mark(1, c.st);
 

@@ -91,16 +91,16 @@ __device__ inline unsigned long long ssq_term(double v, int e) {
     return q * q;
 }
 
-constexpr int kRowChunk = 64;     // columns per thread in row mode
+constexpr int kRowChunk = 64;     // columns per thread in row mode (at most)
 constexpr int kColChunk = 2048;   // rows per block in column mode
 
 template <ElemType ET>
-__global__ __launch_bounds__(256) void amax_rows(int rows, int cols, const void *X, int ld,
+__global__ __launch_bounds__(256) void amax_rows(int rows, int cols, int chunk, const void *X, int ld,
                                                  unsigned long long *amax) {
     const int r = blockIdx.x * 256 + threadIdx.x;
     if (r >= rows) return;
-    const int c0 = blockIdx.y * kRowChunk;
-    const int c1 = min(cols, c0 + kRowChunk);
+    const int c0 = blockIdx.y * chunk;
+    const int c1 = min(cols, c0 + chunk);
     unsigned long long best = 0;
     for (int c = c0; c < c1; ++c) {
         unsigned long long b = Elem<ET>::bits(X, (size_t)r + (size_t)c * ld);
@@ -131,14 +131,14 @@ __global__ __launch_bounds__(256) void amax_cols(int rows, int cols, const void 
 // Cauchy-Schwarz sums of squares (exact in uint64: at most 2 * 2^40 per entry
 // and k <= 149130 entries, below 2^59).  Same traversal as the maxima.
 template <ElemType ET>
-__global__ __launch_bounds__(256) void ssq_rows(int rows, int cols, const void *X, int ld, const int32_t *E,
-                                                unsigned long long *U) {
+__global__ __launch_bounds__(256) void ssq_rows(int rows, int cols, int chunk, const void *X, int ld,
+                                                const int32_t *E, unsigned long long *U) {
     const int r = blockIdx.x * 256 + threadIdx.x;
     if (r >= rows) return;
     const int e = E[r];
     if (e == INT32_MIN) return;
-    const int c0 = blockIdx.y * kRowChunk;
-    const int c1 = min(cols, c0 + kRowChunk);
+    const int c0 = blockIdx.y * chunk;
+    const int c1 = min(cols, c0 + chunk);
     unsigned long long acc = 0;
     for (int c = c0; c < c1; ++c) {
         double v[2];
@@ -170,9 +170,13 @@ __global__ __launch_bounds__(256) void ssq_cols(int rows, int cols, const void *
 
 // E_r -> E_r - 20 + d, d = smallest d >= 0 with 4^d >= U_r, i.e.
 // d = ceil(bitlength(U_r - 1) / 2); then ||row r||_2 <= 2^(new E_r).
-__global__ void cs_exponents_kernel(int count, const unsigned long long *U, int32_t *E) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= count) return;
+// Entries [0, ca) of (Ua, Ea), then [0, cb) of (Ub, Eb), in one launch.
+__global__ void cs_exponents_kernel(int ca, const unsigned long long *Ua, int32_t *Ea, int cb,
+                                    const unsigned long long *Ub, int32_t *Eb) {
+    int i = blockIdx.x * 256 + threadIdx.x;
+    const unsigned long long *U = Ua;
+    int32_t *E = Ea;
+    if (i >= ca) { i -= ca; U = Ub; E = Eb; if (i >= cb) return; }
     const int e = E[i];
     const unsigned long long u = U[i];
     if (e == INT32_MIN || u == 0) return;
@@ -180,9 +184,13 @@ __global__ void cs_exponents_kernel(int count, const unsigned long long *U, int3
     E[i] = e - 20 + (bits + 1) / 2;
 }
 
-__global__ void exponents_kernel(int count, const unsigned long long *amax, int32_t *E) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= count) return;
+// Entries [0, ca) of (amax_a, Ea), then [0, cb) of (amax_b, Eb), in one launch.
+__global__ void exponents_kernel(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
+                                 const unsigned long long *amax_b, int32_t *Eb) {
+    int i = blockIdx.x * 256 + threadIdx.x;
+    const unsigned long long *amax = amax_a;
+    int32_t *E = Ea;
+    if (i >= ca) { i -= ca; amax = amax_b; E = Eb; if (i >= cb) return; }
     const unsigned long long b = amax[i];
     int e;
     if (b >= 0x7FF0000000000000ull) e = INT32_MIN;      // Inf or NaN in the row
@@ -206,16 +214,26 @@ __global__ void zero_matrix_kernel(unsigned char *c, int rows_bytes, int n, size
 
 }  // namespace
 
+// Columns per thread in row mode: kRowChunk, fewer (down to 8) when the
+// grid would otherwise hold fewer than ~2048 blocks (small matrices).
+int row_chunk(int rows, int cols) {
+    const long rb = (rows + 255) / 256;
+    int chunk = kRowChunk;
+    while (chunk > 8 && rb * ((cols + chunk - 1) / chunk) < 2048) chunk >>= 1;
+    return chunk;
+}
+
 hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X, int ld,
                        unsigned long long *amax, hipStream_t st) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
     if (mode == 0) {
-        dim3 grid((rows + 255) / 256, (cols + kRowChunk - 1) / kRowChunk);
+        const int chunk = row_chunk(rows, cols);
+        dim3 grid((rows + 255) / 256, (cols + chunk - 1) / chunk);
         switch (et) {
-        case kF64: amax_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
-        case kF32: amax_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
-        case kI32: amax_rows<kI32><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
-        case kR64: amax_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, amax); break;
+        case kF64: amax_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, amax); break;
+        case kF32: amax_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, amax); break;
+        case kI32: amax_rows<kI32><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, amax); break;
+        case kR64: amax_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, amax); break;
         }
     } else {
         dim3 grid(cols, (rows + kColChunk - 1) / kColChunk);
@@ -229,9 +247,11 @@ hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X,
     return hipGetLastError();
 }
 
-hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st) {
+hipError_t launch_exponents(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
+                            const unsigned long long *amax_b, int32_t *Eb, hipStream_t st) {
+    const int count = ca + cb;
     if (count <= 0) return hipSuccess;
-    exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(count, amax, E);
+    exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(ca, amax_a, Ea, cb, amax_b, Eb);
     return hipGetLastError();
 }
 
@@ -239,11 +259,12 @@ hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, 
                       unsigned long long *U, hipStream_t st) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
     if (mode == 0) {
-        dim3 grid((rows + 255) / 256, (cols + kRowChunk - 1) / kRowChunk);
+        const int chunk = row_chunk(rows, cols);
+        dim3 grid((rows + 255) / 256, (cols + chunk - 1) / chunk);
         switch (et) {
-        case kF64: ssq_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
-        case kF32: ssq_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
-        case kR64: ssq_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, E, U); break;
+        case kF64: ssq_rows<kF64><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, E, U); break;
+        case kF32: ssq_rows<kF32><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, E, U); break;
+        case kR64: ssq_rows<kR64><<<grid, 256, 0, st>>>(rows, cols, chunk, X, ld, E, U); break;
         default: return hipErrorInvalidValue;
         }
     } else {
@@ -258,9 +279,11 @@ hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, 
     return hipGetLastError();
 }
 
-hipError_t launch_cs_exponents(int count, const unsigned long long *U, int32_t *E, hipStream_t st) {
+hipError_t launch_cs_exponents(int ca, const unsigned long long *Ua, int32_t *Ea, int cb,
+                               const unsigned long long *Ub, int32_t *Eb, hipStream_t st) {
+    const int count = ca + cb;
     if (count <= 0) return hipSuccess;
-    cs_exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(count, U, E);
+    cs_exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(ca, Ua, Ea, cb, Ub, Eb);
     return hipGetLastError();
 }
 

@@ -124,15 +124,18 @@ enum ElemType { kF64 = 0, kF32 = 1, kI32 = 2, kR64 = 3 /* real fp64 */ };
 // matrix, into amax bits (uint64, atomicMax of |x| bit patterns).
 hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X, int ld,
                        unsigned long long *amax, hipStream_t st);
-// K1 finish: amax bits -> exponents (INT32_MIN when non-finite).
-hipError_t launch_exponents(int count, const unsigned long long *amax, int32_t *E, hipStream_t st);
+// K1 finish: amax bits -> exponents (INT32_MIN when non-finite), for ca rows
+// of A and cb columns of B in one launch.
+hipError_t launch_exponents(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
+                            const unsigned long long *amax_b, int32_t *Eb, hipStream_t st);
 // K1, Cauchy-Schwarz rule: U_r += sum over the parts v of row (mode 0) or
 // column (mode 1) r of ceil(|v| 2^(20 - E_r))^2 (exact uint64 atomics; rows
 // with E_r = INT32_MIN are skipped), then E_r += d - 20 with d the smallest
 // d >= 0 such that 4^d >= U_r (U_r = 0 leaves E_r).
 hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, int ld, const int32_t *E,
                       unsigned long long *U, hipStream_t st);
-hipError_t launch_cs_exponents(int count, const unsigned long long *U, int32_t *E, hipStream_t st);
+hipError_t launch_cs_exponents(int ca, const unsigned long long *Ua, int32_t *Ea, int cb,
+                               const unsigned long long *Ub, int32_t *Eb, hipStream_t st);
 
 // K2: quantize + residues + 2M pre into operand planes.
 //   mode 0: operand rows are rows of X (A, m x k), element (r, kk) at X[r + kk*ld]
