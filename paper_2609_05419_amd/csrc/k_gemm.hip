@@ -19,7 +19,10 @@
 // global->LDS loads (global_load_lds_dwordx4, no register staging) into a ring
 // of 4 stages (128 KB of the 160 KB LDS), so loads run 3 stages ahead of the
 // MFMAs.  Each wave reads an operand fragment with one ds_read_b128 (64 lanes
-// x 16 contiguous bytes: no bank conflicts).
+// x 16 contiguous bytes: no bank conflicts).  The two waves of a SIMD meet at
+// a barrier every stage, so whatever they issue between MFMA batches leaves
+// the MFMA pipe idle: the steady-state loop is kept free of branches and
+// conditional waits, and the residues leave straight from the accumulators.
 
 // Bound: int8 MFMA.  Algorithmic work per launch = 2 m n k int8 ops per
 // product (counting the padded-free m, n, k of the problem).
@@ -34,10 +37,7 @@ constexpr int kThreads = 512;                    // 8 waves: 2 per SIMD
 constexpr int kStages = 4;                       // LDS ring of k-stages (32 KB each)
 constexpr int kStageBuf = 2 * kStageBytes;       // A and B of one stage
 constexpr int kLoadsPerStage = 4;                // 16-byte direct loads per thread per stage
-constexpr int kEpiStride = 272;  // bytes per column of the staged 256 x 256 output tile
 constexpr int kPipeBytes = kStages * kStageBuf;
-constexpr int kEpiBytes = 256 * kEpiStride;
-constexpr int kLdsBytes = kPipeBytes > kEpiBytes ? kPipeBytes : kEpiBytes;
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
 constexpr int kGroupRows = 8;
 
@@ -137,8 +137,55 @@ __device__ inline void mfma_half(v4i (&acc)[8][4], const v4i (&a)[8], const v4i 
             acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
 }
 
+// 4 x 4 transpose of dwords across the four 16-lane rows of a wave: on entry
+// row r of d[q] holds X[r][q], on exit row r of d[q] holds X[q][r].
+// v_permlane32_swap exchanges the upper 32 lanes of its first operand with the
+// lower 32 lanes of its second, v_permlane16_swap the odd rows of its first
+// operand with the even rows of its second.
+__device__ inline void transpose_rows(uint32_t (&d)[4]) {
+    auto t02 = __builtin_amdgcn_permlane32_swap(d[0], d[2], false, false);
+    auto t13 = __builtin_amdgcn_permlane32_swap(d[1], d[3], false, false);
+    auto t01 = __builtin_amdgcn_permlane16_swap(t02[0], t13[0], false, false);
+    auto t23 = __builtin_amdgcn_permlane16_swap(t02[1], t13[1], false, false);
+    d[0] = t01[0];
+    d[1] = t01[1];
+    d[2] = t23[0];
+    d[3] = t23[1];
+}
+
+// Epilogue: C mod m -> int8, stored from the accumulators.
+// v_mfma_i32_16x16x64_i8 leaves column (lane % 16), rows 4 (lane / 16) + e of
+// its 16 x 16 block in element e: 4 consecutive rows of the column-major
+// output make one dword.  A transpose across the lane rows of four row blocks
+// gives each lane 16 consecutive rows of one block, so one 16-byte store per
+// lane writes 64 contiguous bytes of each of 16 columns, and the two halves of
+// the wave tile fill whole 128-byte column segments.
+__device__ inline void store_tile(const v4i (&acc)[8][4], int8_t *C, int ldc, int m, double inv) {
+    const uint32_t negm = (uint32_t)(-m) & 0xFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t d[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                uint32_t by[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int v = acc[4 * h + q][j][e];
+                    const double qm = fma((double)v, inv, kMagic);  // 1.5 2^52 + rint(v / m)
+                    by[e] = mad24(lo32(qm), negm, (uint32_t)v);    // v - q m (low byte)
+                }
+                d[q] = pack4(by[0], by[1], by[2], by[3]);
+            }
+            transpose_rows(d);
+            *reinterpret_cast<uint4 *>(C + (size_t)(j * 16) * ldc + h * 64) = uint4{d[0], d[1], d[2], d[3]};
+        }
+    }
+}
+
 __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
-    __shared__ __attribute__((aligned(1024))) int8_t lds[kLdsBytes];
+    __shared__ __attribute__((aligned(1024))) int8_t lds[kPipeBytes];
 
     const TileCoord tc = tile_of((int)blockIdx.x, g.mt, g.nt, g.chunk);
     if (!tc.valid) return;  // whole workgroup: no barrier is pending
@@ -178,17 +225,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     // One k-stage: rows 4..7 of A are read while the MFMAs of rows 0..3 run;
     // the barrier that frees this stage's buffer sits between the two MFMA
     // halves; the next stage's rows 0..3 of A and its B are read while the
-    // MFMAs of rows 4..7 run, and the freed buffer is refilled after them.  The last stage is peeled off so that every
-    // iteration has the same LDS-counter state (no conservative waits).
-    for (int kb = 0; kb + 1 < KB; ++kb) {
+    // MFMAs of rows 4..7 run, and the freed buffer is refilled after them.
+    // `younger` is the number of stages after the next one whose loads may
+    // stay in flight at the barrier; `refill` whether stage kb + 4 exists.
+    auto stage = [&](int kb, int younger, bool refill) {
         const int8_t *buf = lds + (kb % kStages) * kStageBuf;
         wait_lds();
         read_a(buf, wr, lane, 4, fa);
         sched_fence();
         mfma_half(acc, fa, fb, 0);
         sched_fence();
-        // stage kb+1 must have landed; stages kb+2, kb+3 may stay in flight
-        const int younger = min(KB - 1, kb + kStages - 1) - (kb + 1);
         if (younger >= 2) wait_vm<2 * kLoadsPerStage>();
         else if (younger == 1) wait_vm<kLoadsPerStage>();
         else wait_vm<0>();
@@ -201,48 +247,26 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
         sched_fence();
         // refill the freed buffer after the MFMAs, so that the fragment reads
         // above are not queued behind the stage copy
-        if (kb + kStages < KB)
+        if (refill)
             load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
                        lds + (kb % kStages) * kStageBuf, tid, wave);
 #pragma unroll
         for (int j = 0; j < 4; ++j) fb[j] = nb[j];
-    }
+    };
+    // Steady state (constant wait, always a refill), then the last stages
+    // with shrinking waits.  The final stage is peeled off so that every
+    // iteration has the same LDS-counter state (no conservative waits).
+    int kb = 0;
+    for (; kb + kStages < KB; ++kb) stage(kb, 2, true);
+    for (; kb + 1 < KB; ++kb) stage(kb, min(KB - 1, kb + kStages - 1) - (kb + 1), false);
     wait_lds();
     read_a(lds + ((KB - 1) % kStages) * kStageBuf, wr, lane, 4, fa);
     mfma_half(acc, fa, fb, 0);
     mfma_half(acc, fa, fb, 4);
 
-    // ---- epilogue: C mod m -> int8, staged through LDS, coalesced store ----
-    // v_mfma_i32_16x16x64_i8 leaves column (lane % 16), rows 4 (lane / 16) + e
-    // of its 16 x 16 block in element e: 4 consecutive rows make one dword.
-    stage_barrier();  // every wave is done with the ring; no loads are in flight
-    const double inv = g.inv[p];
-    const uint32_t negm = (uint32_t)(-g.mod[p]) & 0xFFFFFFu;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            uint32_t by[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int v = acc[i][j][e];
-                const double q = fma((double)v, inv, kMagic);   // 1.5 2^52 + rint(v / m)
-                by[e] = mad24(lo32(q), negm, (uint32_t)v);     // v - q m (low byte)
-            }
-            const int col = wc * 64 + j * 16 + (lane & 15);
-            const int row = wr * 128 + i * 16 + 4 * (lane >> 4);
-            *reinterpret_cast<uint32_t *>(lds + col * kEpiStride + row) = pack4(by[0], by[1], by[2], by[3]);
-        }
-    }
-    __syncthreads();
-    int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256) * g.ldc + ti * 256;
-    const int ch = tid & 15;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int c = (tid >> 4) + 32 * q;
-        *reinterpret_cast<uint4 *>(C + (size_t)c * g.ldc + ch * 16) =
-            *reinterpret_cast<const uint4 *>(lds + c * kEpiStride + ch * 16);
-    }
+    int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256 + wc * 64 + (lane & 15)) * g.ldc + ti * 256 +
+                wr * 128 + 16 * (lane >> 4);
+    store_tile(acc, C, g.ldc, g.mod[p], g.inv[p]);
 }
 
 }  // namespace
