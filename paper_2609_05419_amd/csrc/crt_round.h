@@ -96,22 +96,28 @@ O2M_HD inline double round_words(UW<W> v, int sc) {
             v.w[i] = t;
         }
     }
-    int top = -1;  // index of the most significant nonzero word
+    // the most significant nonzero word (hi), the word below it (lo) and the
+    // OR of all lower words; every index is static, so the words stay in
+    // registers
+    int top = -1;
+    uint64_t hi = 0, lo = 0, low = 0;
 #pragma unroll
-    for (int i = W - 1; i >= 0; --i)
-        if (top < 0 && v.w[i]) top = i;
-    if (top < 0) return 0.0;
-    const int lz = clz64(v.w[top]);
-    // h = the 64 bits below the leading one (inclusive), rest = sticky bits
-    uint64_t h = v.w[top] << lz;
-    uint64_t rest = 0;
-    if (top > 0) {
-        if (lz) h |= v.w[top - 1] >> (64 - lz);
-        rest = v.w[top - 1] << lz;
-#pragma unroll
-        for (int i = 0; i < W; ++i)
-            if (i < top - 1) rest |= v.w[i];
+    for (int i = W - 1; i >= 0; --i) {
+        if (top < 0 && v.w[i] != 0) {
+            top = i;
+            hi = v.w[i];
+            lo = i > 0 ? v.w[i > 0 ? i - 1 : 0] : 0;
+        }
     }
+    if (top < 0) return 0.0;
+#pragma unroll
+    for (int i = 0; i + 2 < W; ++i)
+        if (i < top - 1) low |= v.w[i];
+    const int lz = clz64(hi);
+    // h = the 64 bits below the leading one (inclusive), rest = sticky bits
+    uint64_t h = hi << lz;
+    if (lz) h |= lo >> (64 - lz);
+    const uint64_t rest = (lo << lz) | low;
     uint64_t mant = h >> 11;
     const uint64_t rb = h & 0x7FF;
     if (rb > 0x400 || (rb == 0x400 && (rest != 0 || (mant & 1)))) mant += 1;
@@ -145,6 +151,7 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     } else {
         constexpr int W = LimbWords<T>::value;
         UW<W> v = {};
+#pragma unroll
         for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)c[t], 40 * t);
         return round_words<W>(v, sc);
     }
@@ -158,6 +165,7 @@ O2M_HD inline UW<LimbWords<T>::value> lift_exact(const double (&S)[T], const dou
     const double q = rint(X * inv_m);
     constexpr int W = LimbWords<T>::value;
     UW<W> v = {};
+#pragma unroll
     for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)fma(-q, mlimb[t], S[t]), 40 * t);
     return v;
 }
