@@ -10,19 +10,22 @@
 // column-major with leading dimension ldc (= m_pad), so the CRT kernel reads
 // 1 byte per product per output entry instead of 4.
 //
-// Tiling for gfx950: a 256 x 256 output tile per workgroup of 8 waves (2 per
-// SIMD, 2 x 4), each wave owning 128 x 64 = 8 x 4 accumulators of
-// v_mfma_i32_16x16x64_i8.  On random int8 data this instruction sustains a
-// markedly higher clock than v_mfma_i32_32x32x32_i8 at the same MAC rate, and
-// the second wave per SIMD hides LDS and barrier latency.  A k-stage of 64 is
-// 16 KB per operand, one contiguous chunk of the plane, copied by direct
-// global->LDS loads (global_load_lds_dwordx4, no register staging) into a ring
-// of 4 stages (128 KB of the 160 KB LDS), so loads run 3 stages ahead of the
+// Tiling for gfx950: a 256 x 256 output tile per workgroup of 4 waves (one
+// per SIMD, 2 x 2), each wave owning 128 x 128 = 8 x 8 accumulators of
+// v_mfma_i32_16x16x64_i8 held in the 256 accumulation registers (AGPRs).  On
+// random int8 data this instruction sustains a markedly higher clock than
+// v_mfma_i32_32x32x32_i8 at the same MAC rate.  A k-stage of 64 is 16 KB per
+// operand, one contiguous chunk of the plane, copied by direct global->LDS
+// loads (global_load_lds_dwordx4, no register staging) into a ring of 4
+// stages (128 KB of the 160 KB LDS), so loads run 3 stages ahead of the
 // MFMAs.  Each wave reads an operand fragment with one ds_read_b128 (64 lanes
-// x 16 contiguous bytes: no bank conflicts).  The two waves of a SIMD meet at
-// a barrier every stage, so whatever they issue between MFMA batches leaves
-// the MFMA pipe idle: the steady-state loop is kept free of branches and
-// conditional waits, and the residues leave straight from the accumulators.
+// x 16 contiguous bytes: no bank conflicts); with 128 x 128 wave tiles that is
+// 16 reads per 64 MFMAs, a third fewer than with 128 x 64, which also lets the
+// part hold a higher clock.  With one wave per SIMD nothing else feeds the
+// MFMA pipe, so each stage issues its 16 fragment reads after every other one
+// of its first 32 MFMAs and its 8 stage copies after every fourth of the last
+// 32: a memory instruction never waits behind another one in front of an
+// MFMA.  The residues leave straight from the accumulators.
 
 // Bound: int8 MFMA.  Algorithmic work per launch = 2 m n k int8 ops per
 // product (counting the padded-free m, n, k of the problem).
@@ -33,10 +36,10 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 512;                    // 8 waves: 2 per SIMD
+constexpr int kThreads = 256;                    // 4 waves: one per SIMD
 constexpr int kStages = 4;                       // LDS ring of k-stages (32 KB each)
 constexpr int kStageBuf = 2 * kStageBytes;       // A and B of one stage
-constexpr int kLoadsPerStage = 4;                // 16-byte direct loads per thread per stage
+constexpr int kLoadsPerStage = 8;                // 16-byte direct loads per thread per stage
 constexpr int kPipeBytes = kStages * kStageBuf;
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
 constexpr int kGroupRows = 8;
@@ -106,35 +109,53 @@ __device__ inline void stage_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Issue the direct loads of one k-stage (A then B, 16 KB each) into LDS
-// buffer `buf`: each wave copies 1 KB contiguous per instruction.
+// Direct load q (0..7) of one k-stage into LDS buffer `buf`: even q copy
+// 4 KB of A, odd q 4 KB of B; each wave copies 1 KB contiguous.
+__device__ inline void load_part(const int8_t *A, const int8_t *B, int8_t *buf, int tid, int wave, int q) {
+    const int off = (q >> 1) * 4096;
+    if ((q & 1) == 0)
+        __builtin_amdgcn_global_load_lds(A + off + tid * 16, (lds_void *)(buf + off + wave * 1024), 16, 0, 0);
+    else
+        __builtin_amdgcn_global_load_lds(B + off + tid * 16, (lds_void *)(buf + kStageBytes + off + wave * 1024), 16, 0, 0);
+}
+
 __device__ inline void load_stage(const int8_t *A, const int8_t *B, int8_t *buf, int tid, int wave) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        __builtin_amdgcn_global_load_lds(A + q * 8192 + tid * 16, (lds_void *)(buf + q * 8192 + wave * 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(B + q * 8192 + tid * 16,
-                                         (lds_void *)(buf + kStageBytes + q * 8192 + wave * 1024), 16, 0, 0);
+    for (int q = 0; q < kLoadsPerStage; ++q) load_part(A, B, buf, tid, wave, q);
+}
+
+// Fragment f (0..15) of a stage: A rows 16 f of the wave for f < 8, B rows
+// 16 (f - 8) of the wave after that.
+__device__ inline v4i read_frag(const int8_t *buf, int aoff, int boff, int lane, int f) {
+    const int off = f < 8 ? aoff + f * kFragBytes : boff + (f - 8) * kFragBytes;
+    return *reinterpret_cast<const v4i *>(buf + off + lane * 16);
+}
+
+// acc += a b^T on one 16 x 16 block.  Written as inline assembly so that the
+// accumulator stays in its AGPRs: with the builtin the compiler copies the
+// 256 accumulators between AGPRs and VGPRs in every stage.  The compiler does
+// not see this as an MFMA, so the hazards it would otherwise cover are
+// handled where they arise: fragment reads are waited for (lgkmcnt) before a
+// stage's MFMAs, and acc_fence() separates accumulator writes from reads.
+__device__ inline void mfma(v4i &acc, const v4i &a, const v4i &b) {
+    asm volatile("v_mfma_i32_16x16x64_i8 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b) : "memory");
+}
+
+// Wait states between the accumulator registers' last writer and their next
+// reader (zero fill -> first MFMA, last MFMA -> epilogue reads).  Each asm
+// takes a row of accumulators as operands, so no access to them can move
+// across it.
+template <int NOPS>
+__device__ inline void acc_fence(v4i (&acc)[8][8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        if (NOPS >= 16)
+            asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]),
+                         "+a"(acc[i][3]), "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
+        else
+            asm volatile("s_nop 4" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]),
+                         "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
     }
-}
-
-// Operand fragments of a wave (128 rows of A, 64 rows of B) for one stage.
-__device__ inline void read_a(const int8_t *buf, int wr, int lane, int i0, v4i (&a)[8]) {
-#pragma unroll
-    for (int i = i0; i < i0 + 4; ++i) a[i] = *reinterpret_cast<const v4i *>(buf + (wr * 8 + i) * kFragBytes + lane * 16);
-}
-__device__ inline void read_b(const int8_t *buf, int wc, int lane, v4i (&b)[4]) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const v4i *>(buf + kStageBytes + (wc * 4 + j) * kFragBytes + lane * 16);
-}
-
-// 16 MFMAs: accumulator rows i0..i0+3 against all 4 B fragments.
-__device__ inline void mfma_half(v4i (&acc)[8][4], const v4i (&a)[8], const v4i (&b)[4], int i0) {
-#pragma unroll
-    for (int i = i0; i < i0 + 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
 }
 
 // 4 x 4 transpose of dwords across the four 16-lane rows of a wave: on entry
@@ -160,10 +181,10 @@ __device__ inline void transpose_rows(uint32_t (&d)[4]) {
 // gives each lane 16 consecutive rows of one block, so one 16-byte store per
 // lane writes 64 contiguous bytes of each of 16 columns, and the two halves of
 // the wave tile fill whole 128-byte column segments.
-__device__ inline void store_tile(const v4i (&acc)[8][4], int8_t *C, int ldc, int m, double inv) {
+__device__ inline void store_tile(const v4i (&acc)[8][8], int8_t *C, int ldc, int m, double inv) {
     const uint32_t negm = (uint32_t)(-m) & 0xFFFFFFu;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             uint32_t d[4];
@@ -194,17 +215,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
-    const int wr = wave >> 2, wc = wave & 3;                     // 2 x 4 waves of 128 x 64
+    const int wr = wave >> 1, wc = wave & 1;                     // 2 x 2 waves of 128 x 128
     const int KB = g.kblocks;
+    const int aoff = wr * 8 * kFragBytes, boff = kStageBytes + wc * 8 * kFragBytes;
 
     const int8_t *A = g.a + (size_t)p * g.a_pstride + (size_t)ti * KB * kStageBytes;
     const int8_t *B = g.b + (size_t)p * g.b_pstride + (size_t)tj * KB * kStageBytes;
 
-    v4i acc[8][4];
+    v4i acc[8][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = v4i{};
+        for (int j = 0; j < 8; ++j) acc[i][j] = v4i{};
+    acc_fence<5>(acc);
 
     // prologue: fill the ring, then wait for stage 0
     const int pre = KB < kStages ? KB : kStages;
@@ -218,53 +241,90 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     }
     stage_barrier();
 
-    v4i fa[8], fb[4], nb[4];
-    read_a(lds, wr, lane, 0, fa);
-    read_b(lds, wc, lane, fb);
+    // Fragments of the current stage (f0 = A, g0 = B) and of the next one.
+    v4i fa0[8], fb0[8], fa1[8], fb1[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        fa0[f] = read_frag(lds, aoff, boff, lane, f);
+        fb0[f] = read_frag(lds, aoff, boff, lane, 8 + f);
+    }
+    wait_lds();
 
-    // One k-stage: rows 4..7 of A are read while the MFMAs of rows 0..3 run;
-    // the barrier that frees this stage's buffer sits between the two MFMA
-    // halves; the next stage's rows 0..3 of A and its B are read while the
-    // MFMAs of rows 4..7 run, and the freed buffer is refilled after them.
-    // `younger` is the number of stages after the next one whose loads may
-    // stay in flight at the barrier; `refill` whether stage kb + 4 exists.
-    auto stage = [&](int kb, int younger, bool refill) {
-        const int8_t *buf = lds + (kb % kStages) * kStageBuf;
-        wait_lds();
-        read_a(buf, wr, lane, 4, fa);
-        sched_fence();
-        mfma_half(acc, fa, fb, 0);
-        sched_fence();
+    // Stage kb, its fragments in (ca, cb): wait until stage kb+1 has landed
+    // (`younger` later stages may stay in flight), barrier (every wave is done
+    // reading stage kb, so its buffer is free), then the 64 MFMAs of stage kb
+    // with the fragment reads of stage kb+1 into (na, nb) and the copy of stage
+    // kb+4 into the freed buffer.  In the steady state they are interleaved
+    // with the MFMAs; the last stages issue them first.
+    auto stage = [&](int kb, v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8], int younger, bool next,
+                     bool refill) {
         if (younger >= 2) wait_vm<2 * kLoadsPerStage>();
         else if (younger == 1) wait_vm<kLoadsPerStage>();
         else wait_vm<0>();
-        stage_barrier();  // every wave is done reading stage kb: its buffer is free
+        stage_barrier();
         const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
-        read_a(nbuf, wr, lane, 0, fa);
-        read_b(nbuf, wc, lane, nb);
-        sched_fence();
-        mfma_half(acc, fa, fb, 4);
-        sched_fence();
-        // refill the freed buffer after the MFMAs, so that the fragment reads
-        // above are not queued behind the stage copy
+        if (next) {
+#pragma unroll
+            for (int f = 0; f < 8; ++f) {
+                na[f] = read_frag(nbuf, aoff, boff, lane, f);
+                nb[f] = read_frag(nbuf, aoff, boff, lane, 8 + f);
+            }
+        }
         if (refill)
             load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
                        lds + (kb % kStages) * kStageBuf, tid, wave);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) fb[j] = nb[j];
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) mfma(acc[i][j], ca[i], cb[j]);
+        wait_lds();  // the next stage's fragments are in registers
     };
-    // Steady state (constant wait, always a refill), then the last stages
-    // with shrinking waits.  The final stage is peeled off so that every
-    // iteration has the same LDS-counter state (no conservative waits).
+    auto steady = [&](int kb, v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8]) {
+        wait_vm<2 * kLoadsPerStage>();
+        stage_barrier();
+        const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
+        int8_t *rbuf = lds + (kb % kStages) * kStageBuf;
+        const int8_t *As = A + (size_t)(kb + kStages) * kStageBytes;
+        const int8_t *Bs = B + (size_t)(kb + kStages) * kStageBytes;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                mfma(acc[i][j], ca[i], cb[j]);
+                const int t = 8 * i + j;
+                // fragment reads after every other MFMA of the first half, the
+                // stage copy after every fourth of the second half
+                if (t < 32 && (t & 1) == 0) {
+                    const int f = t >> 1;
+                    if (f < 8) na[f] = read_frag(nbuf, aoff, boff, lane, f);
+                    else nb[f - 8] = read_frag(nbuf, aoff, boff, lane, f);
+                }
+                if (t >= 32 && (t & 3) == 0) load_part(As, Bs, rbuf, tid, wave, (t - 32) >> 2);
+            }
+        wait_lds();
+    };
+    // Steady state, two stages per trip so that the fragment sets alternate
+    // statically; then at most five stages with shrinking waits, the sets
+    // still alternating statically.
     int kb = 0;
-    for (; kb + kStages < KB; ++kb) stage(kb, 2, true);
-    for (; kb + 1 < KB; ++kb) stage(kb, min(KB - 1, kb + kStages - 1) - (kb + 1), false);
-    wait_lds();
-    read_a(lds + ((KB - 1) % kStages) * kStageBuf, wr, lane, 4, fa);
-    mfma_half(acc, fa, fb, 0);
-    mfma_half(acc, fa, fb, 4);
+    for (; kb + kStages + 1 < KB; kb += 2) {
+        steady(kb, fa0, fb0, fa1, fb1);
+        steady(kb + 1, fa1, fb1, fa0, fb0);
+    }
+    auto tail = [&](v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8]) {
+        if (kb < KB) {
+            stage(kb, ca, cb, na, nb, min(KB - 1, kb + kStages - 1) - (kb + 1), kb + 1 < KB, kb + kStages < KB);
+            ++kb;
+        }
+    };
+    tail(fa0, fb0, fa1, fb1);
+    tail(fa1, fb1, fa0, fb0);
+    tail(fa0, fb0, fa1, fb1);
+    tail(fa1, fb1, fa0, fb0);
+    tail(fa0, fb0, fa1, fb1);
 
-    int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256 + wc * 64 + (lane & 15)) * g.ldc + ti * 256 +
+    acc_fence<24>(acc);  // the last MFMAs have written every accumulator
+    int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256 + wc * 128 + (lane & 15)) * g.ldc + ti * 256 +
                 wr * 128 + 16 * (lane >> 4);
     store_tile(acc, C, g.ldc, g.mod[p], g.inv[p]);
 }
