@@ -25,6 +25,8 @@
 #include "o2m_internal.h"
 #include "crt_round.h"
 
+#include <type_traits>
+
 namespace o2m {
 namespace {
 
@@ -43,10 +45,11 @@ template <> struct Out<kF32> {
 };
 
 // MODE 0: ZGEMM / CGEMM output.  MODE 3: exact Gaussian integers (int64).
-// MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R
-// consecutive rows of one column (R = 4: one dword per plane; R = 8: two).
-template <int T, int MODE, ElemType OT, int R>
+// MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R = 4
+// consecutive rows of one column: one dword per plane.
+template <int T, int MODE, ElemType OT>
 __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
+    constexpr int R = 4;
     const int rows_per_block = 256 * R;
     const int mblocks = (a.m + rows_per_block - 1) / rows_per_block;
     const int j = blockIdx.x / mblocks;
@@ -89,45 +92,62 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
-    for (int l = 0; l < cp.n2; ++l) {
-        uint32_t wp[R / 4], wm[R / 4];
-        if (R == 8) {
-            const uint2 p2 = *reinterpret_cast<const uint2 *>(base + (size_t)(2 * l) * a.plane_bytes);
-            const uint2 m2 = *reinterpret_cast<const uint2 *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
-            wp[0] = p2.x; wp[R / 4 - 1] = p2.y;
-            wm[0] = m2.x; wm[R / 4 - 1] = m2.y;
-        } else {
-            wp[0] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l) * a.plane_bytes);
-            wm[0] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * l + 1) * a.plane_bytes);
+    // 2M moduli, in chunks whose plane loads are all issued before their limb
+    // sums, so that each wave keeps several loads in flight
+    auto chunk2m = [&](int l0, auto ch) {
+        constexpr int CH = decltype(ch)::value;
+        uint32_t wp[CH], wm[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            wp[c] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * (l0 + c)) * a.plane_bytes);
+            wm[c] = *reinterpret_cast<const uint32_t *>(base + (size_t)(2 * (l0 + c) + 1) * a.plane_bytes);
         }
 #pragma unroll
-        for (int e = 0; e < R; ++e) {
-            const int rp = sext8(wp[e >> 2], e & 3), rm = sext8(wm[e >> 2], e & 3);
-            const double u = (double)(rm + rp), v = (double)(rm - rp);
+        for (int c = 0; c < CH; ++c)
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
-                sre[e][t] = fma(u, cp.wre[l][t], sre[e][t]);
-                sim[e][t] = fma(v, cp.wim[l][t], sim[e][t]);
+            for (int e = 0; e < R; ++e) {
+                const int rp = sext8(wp[c], e), rm = sext8(wm[c], e);
+                const double u = (double)(rm + rp), v = (double)(rm - rp);
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    sre[e][t] = fma(u, cp.wre[l0 + c][t], sre[e][t]);
+                    sim[e][t] = fma(v, cp.wim[l0 + c][t], sim[e][t]);
+                }
             }
-        }
+    };
+    int l = 0;
+    for (; l + 8 <= cp.n2; l += 8) chunk2m(l, std::integral_constant<int, 8>());
+    if (l + 4 <= cp.n2) {
+        chunk2m(l, std::integral_constant<int, 4>());
+        l += 4;
     }
-    // 3M moduli of a hybrid set: Re = T1 - T2, Im = T3 - T1 - T2, plain weights
-    for (int l = cp.n2; l < cp.n; ++l) {
-        const size_t p0 = (size_t)(2 * cp.n2 + 3 * (l - cp.n2));
-        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(base + p0 * a.plane_bytes);
-        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(base + (p0 + 1) * a.plane_bytes);
-        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(base + (p0 + 2) * a.plane_bytes);
+    for (; l < cp.n2; ++l) chunk2m(l, std::integral_constant<int, 1>());
+    // 3M moduli of a hybrid set: Re = T1 - T2, Im = T3 - T1 - T2, plain
+    // weights; loads issued per chunk as above
+    auto chunk3m = [&](int l0, auto ch) {
+        constexpr int CH = decltype(ch)::value;
+        uint32_t w[CH][3];
 #pragma unroll
-        for (int e = 0; e < R; ++e) {
-            const int t1 = sext8(w1, e & 3), t2 = sext8(w2, e & 3), t3 = sext8(w3, e & 3);
-            const double u = (double)(t1 - t2), v = (double)(t3 - t1 - t2);
+        for (int c = 0; c < CH; ++c) {
+            const size_t p0 = (size_t)(2 * cp.n2 + 3 * (l0 + c - cp.n2));
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
-                sre[e][t] = fma(u, cp.wre[l][t], sre[e][t]);
-                sim[e][t] = fma(v, cp.wre[l][t], sim[e][t]);
+            for (int q = 0; q < 3; ++q) w[c][q] = *reinterpret_cast<const uint32_t *>(base + (p0 + q) * a.plane_bytes);
+        }
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int e = 0; e < R; ++e) {
+                const int t1 = sext8(w[c][0], e), t2 = sext8(w[c][1], e), t3 = sext8(w[c][2], e);
+                const double u = (double)(t1 - t2), v = (double)(t3 - t1 - t2);
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    sre[e][t] = fma(u, cp.wre[l0 + c][t], sre[e][t]);
+                    sim[e][t] = fma(v, cp.wre[l0 + c][t], sim[e][t]);
+                }
             }
-        }
-    }
+    };
+    for (; l + 2 <= cp.n; l += 2) chunk3m(l, std::integral_constant<int, 2>());
+    for (; l < cp.n; ++l) chunk3m(l, std::integral_constant<int, 1>());
 
 #pragma unroll
     for (int e = 0; e < R; ++e) {
@@ -241,16 +261,13 @@ hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &c
         else crt_sym_kernel<T, true><<<blocks, 256, 0, st>>>(ca, cp);
         return hipGetLastError();
     }
-    // 8 rows per thread when the residue rows are 8-byte aligned (ldr is a
-    // multiple of 256) and the limb count leaves room in registers
-    constexpr int R = 4;
-    const long blocks = (long)((ca.m + 256 * R - 1) / (256 * R)) * ca.n;
-    const long blocks4 = (long)((ca.m + 1023) / 1024) * ca.n;
-    if (blocks > 0x7FFFFFFF || blocks4 > 0x7FFFFFFF) return hipErrorInvalidValue;
-    if (mode == 0 && ot == kF64) crt_kernel<T, 0, kF64, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 0 && ot == kF32) crt_kernel<T, 0, kF32, R><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-    else if (mode == 3 && T == 2) crt_kernel<2, 3, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
-    else if (mode == 4) crt_kernel<T, 4, kF64, 4><<<(unsigned)blocks4, 256, 0, st>>>(ca, cp);
+    // 4 rows of one column per thread, 1024 rows per workgroup
+    const long blocks = (long)((ca.m + 1023) / 1024) * ca.n;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (mode == 0 && ot == kF64) crt_kernel<T, 0, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    else if (mode == 0 && ot == kF32) crt_kernel<T, 0, kF32><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    else if (mode == 3 && T == 2) crt_kernel<2, 3, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+    else if (mode == 4) crt_kernel<T, 4, kF64><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
