@@ -136,26 +136,28 @@ __device__ inline v4i read_frag(const int8_t *buf, int aoff, int boff, int lane,
 // 256 accumulators between AGPRs and VGPRs in every stage.  The compiler does
 // not see this as an MFMA, so the hazards it would otherwise cover are
 // handled where they arise: fragment reads are waited for (lgkmcnt) before a
-// stage's MFMAs, and acc_fence() separates accumulator writes from reads.
+// stage's MFMAs, and acc_after_fill() / acc_after_mfma() separate
+// accumulator writes from reads.
 __device__ inline void mfma(v4i &acc, const v4i &a, const v4i &b) {
     asm volatile("v_mfma_i32_16x16x64_i8 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b) : "memory");
 }
 
 // Wait states between the accumulator registers' last writer and their next
-// reader (zero fill -> first MFMA, last MFMA -> epilogue reads).  Each asm
-// takes a row of accumulators as operands, so no access to them can move
-// across it.
-template <int NOPS>
-__device__ inline void acc_fence(v4i (&acc)[8][8]) {
+// reader.  Each asm takes a row of accumulators as operands, so no access to
+// them can move across it.
+//   acc_after_fill: the zero fill (VALU writes) before the first MFMA reads them
+//   acc_after_mfma: the last MFMAs (16 passes) before the epilogue reads them
+__device__ inline void acc_after_fill(v4i (&acc)[8][8]) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        if (NOPS >= 16)
-            asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]),
-                         "+a"(acc[i][3]), "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
-        else
-            asm volatile("s_nop 4" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]),
-                         "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
-    }
+    for (int i = 0; i < 8; ++i)
+        asm volatile("s_nop 4" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]),
+                     "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
+}
+__device__ inline void acc_after_mfma(v4i (&acc)[8][8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        asm volatile("s_nop 7\n s_nop 7\n s_nop 7" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]),
+                     "+a"(acc[i][3]), "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7]));
 }
 
 // 4 x 4 transpose of dwords across the four 16-lane rows of a wave: on entry
@@ -227,7 +229,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = v4i{};
-    acc_fence<5>(acc);
+    acc_after_fill(acc);
 
     // prologue: fill the ring, then wait for stage 0
     const int pre = KB < kStages ? KB : kStages;
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     tail(fa1, fb1, fa0, fb0);
     tail(fa0, fb0, fa1, fb1);
 
-    acc_fence<24>(acc);  // the last MFMAs have written every accumulator
+    acc_after_mfma(acc);
     int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256 + wc * 128 + (lane & 15)) * g.ldc + ti * 256 +
                 wr * 128 + 16 * (lane >> 4);
     store_tile(acc, C, g.ldc, g.mod[p], g.inv[p]);
