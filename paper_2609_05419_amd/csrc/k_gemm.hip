@@ -15,8 +15,8 @@
 // v_mfma_i32_16x16x64_i8 held in the 256 accumulation registers (AGPRs).  On
 // random int8 data this instruction sustains a markedly higher clock than
 // v_mfma_i32_32x32x32_i8 at the same MAC rate.  A k-stage of 64 is 16 KB per
-// operand, one contiguous chunk of the plane, copied by direct global->LDS
-// loads (global_load_lds_dwordx4, no register staging) into a ring of 4
+// operand, one contiguous chunk of the plane, copied by direct buffer->LDS
+// loads (buffer_load_dwordx4 ... lds, no register staging) into a ring of 4
 // stages (128 KB of the 160 KB LDS), so loads run 3 stages ahead of the
 // MFMAs.  Each wave reads an operand fragment with one ds_read_b128 (64 lanes
 // x 16 contiguous bytes: no bank conflicts); with 128 x 128 wave tiles that is
@@ -109,19 +109,34 @@ __device__ inline void stage_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Direct load q (0..7) of one k-stage into LDS buffer `buf`: even q copy
-// 4 KB of A, odd q 4 KB of B; each wave copies 1 KB contiguous.
-__device__ inline void load_part(const int8_t *A, const int8_t *B, int8_t *buf, int tid, int wave, int q) {
-    const int off = (q >> 1) * 4096;
-    if ((q & 1) == 0)
-        __builtin_amdgcn_global_load_lds(A + off + tid * 16, (lds_void *)(buf + off + wave * 1024), 16, 0, 0);
-    else
-        __builtin_amdgcn_global_load_lds(B + off + tid * 16, (lds_void *)(buf + kStageBytes + off + wave * 1024), 16, 0, 0);
+// Raw buffer descriptor over one tile's K-major operand rows (all its
+// k-stages): the copies then take their stage offset from a scalar register
+// and a fixed per-lane offset, with no 64-bit address arithmetic per copy, and
+// a copy beyond the extent would read zeros instead of faulting.
+constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit buffer (gfx9 family)
+
+__device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const int8_t *base, int kblocks) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t *>(base), (short)0, kblocks * kStageBytes,
+                                             kBufferWord3);
 }
 
-__device__ inline void load_stage(const int8_t *A, const int8_t *B, int8_t *buf, int tid, int wave) {
+// Direct copy q (0..7) of k-stage `stage` into LDS buffer `buf`: even q copy
+// 4 KB of A, odd q 4 KB of B; each wave copies 1 KB contiguous.
+__device__ inline void load_part(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB, int stage, int8_t *buf,
+                                 int tid, int wave, int q) {
+    const int off = (q >> 1) * 4096;
+    const int soff = stage * kStageBytes + off;
+    if ((q & 1) == 0)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void *)(buf + off + wave * 1024), 16, tid * 16, soff, 0, 0);
+    else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void *)(buf + kStageBytes + off + wave * 1024), 16,
+                                                 tid * 16, soff, 0, 0);
+}
+
+__device__ inline void load_stage(__amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB, int stage, int8_t *buf,
+                                  int tid, int wave) {
 #pragma unroll
-    for (int q = 0; q < kLoadsPerStage; ++q) load_part(A, B, buf, tid, wave, q);
+    for (int q = 0; q < kLoadsPerStage; ++q) load_part(rA, rB, stage, buf, tid, wave, q);
 }
 
 // Fragment f (0..15) of a stage: A rows 16 f of the wave for f < 8, B rows
@@ -221,8 +236,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     const int KB = g.kblocks;
     const int aoff = wr * 8 * kFragBytes, boff = kStageBytes + wc * 8 * kFragBytes;
 
-    const int8_t *A = g.a + (size_t)p * g.a_pstride + (size_t)ti * KB * kStageBytes;
-    const int8_t *B = g.b + (size_t)p * g.b_pstride + (size_t)tj * KB * kStageBytes;
+    const __amdgpu_buffer_rsrc_t rA = tile_rsrc(g.a + (size_t)p * g.a_pstride + (size_t)ti * KB * kStageBytes, KB);
+    const __amdgpu_buffer_rsrc_t rB = tile_rsrc(g.b + (size_t)p * g.b_pstride + (size_t)tj * KB * kStageBytes, KB);
 
     v4i acc[8][8];
 #pragma unroll
@@ -234,7 +249,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     // prologue: fill the ring, then wait for stage 0
     const int pre = KB < kStages ? KB : kStages;
     for (int s = 0; s < pre; ++s)
-        load_stage(A + (size_t)s * kStageBytes, B + (size_t)s * kStageBytes, lds + s * kStageBuf, tid, wave);
+        load_stage(rA, rB, s, lds + s * kStageBuf, tid, wave);
     switch (pre) {
     case 1: wait_vm<0>(); break;
     case 2: wait_vm<kLoadsPerStage>(); break;
@@ -272,9 +287,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
                 nb[f] = read_frag(nbuf, aoff, boff, lane, 8 + f);
             }
         }
-        if (refill)
-            load_stage(A + (size_t)(kb + kStages) * kStageBytes, B + (size_t)(kb + kStages) * kStageBytes,
-                       lds + (kb % kStages) * kStageBuf, tid, wave);
+        if (refill) load_stage(rA, rB, kb + kStages, lds + (kb % kStages) * kStageBuf, tid, wave);
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -286,8 +299,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
         stage_barrier();
         const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
         int8_t *rbuf = lds + (kb % kStages) * kStageBuf;
-        const int8_t *As = A + (size_t)(kb + kStages) * kStageBytes;
-        const int8_t *Bs = B + (size_t)(kb + kStages) * kStageBytes;
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -301,7 +312,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
                     if (f < 8) na[f] = read_frag(nbuf, aoff, boff, lane, f);
                     else nb[f - 8] = read_frag(nbuf, aoff, boff, lane, f);
                 }
-                if (t >= 32 && (t & 3) == 0) load_part(As, Bs, rbuf, tid, wave, (t - 32) >> 2);
+                if (t >= 32 && (t & 3) == 0) load_part(rA, rB, kb + kStages, rbuf, tid, wave, (t - 32) >> 2);
             }
         wait_lds();
     };
