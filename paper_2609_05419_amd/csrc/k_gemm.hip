@@ -100,7 +100,7 @@ __device__ inline void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 __device__ inline void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Workgroup barrier without a memory fence: the stage data arrives by direct
-// global->LDS loads that each thread has already waited for (vmcnt), and the
+// buffer->LDS loads that each thread has already waited for (vmcnt), and the
 // LDS reads of the stage being recycled have completed (lgkmcnt(0)).
 __device__ inline void stage_barrier() {
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
