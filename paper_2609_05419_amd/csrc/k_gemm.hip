@@ -58,23 +58,30 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
 }
 
 // Tile schedule.  The hardware deals workgroups to the 8 XCDs round-robin
-// (workgroup b -> XCD b % 8, in dispatch order b / 8 within it).  Each batch
-// item (one int8 GEMM) is split into 8 contiguous chunks of its grouped tile
-// order, one per XCD, and all XCDs sweep the batch items in the same order:
-// at any time the whole chip works on one product, whose operand planes
-// (2 x 64 MB at 8192^2) stay resident in the 256 MB Infinity Cache, while the
-// tiles resident on one XCD (8 tile-rows x 4 tile-columns) share their A and
-// B stages in that XCD's L2.  Slots beyond a product's tile count idle.
+// (workgroup b -> XCD b % 8, in dispatch order b / 8 within it), and all XCDs
+// sweep the batch items (one int8 GEMM each) in the same order, so at any time
+// the whole chip works on one product.  Within a product the tiles follow a
+// grouped order (groups of 8 tile-rows, column-major inside a group), cut into
+// windows of 32 tiles (8 tile-rows x 4 tile-columns): the tiles resident on
+// one XCD at a time share their A and B stages in that XCD's L2.  Small
+// products give each XCD one contiguous chunk of the order.  Large ones deal
+// the windows round-robin (window w -> XCD w % 8), so that all XCDs work in
+// the same group of 8 tile-rows at once: its A strip is read once from HBM
+// and shared through the 256 MB Infinity Cache even when a product's planes
+// (2 x 256 MB at 16384^2) do not fit in it.  Slots beyond a product's tiles
+// idle.
 struct TileCoord {
     int p, ti, tj;
     bool valid;
 };
-__device__ inline TileCoord tile_of(int b, int mt, int nt, int chunk) {
+__device__ inline TileCoord tile_of(int b, int mt, int nt, int chunk, int deal) {
     TileCoord c;
     const int x = b & 7, slot = b >> 3;
     c.p = slot / chunk;
-    const int t = x * chunk + (slot - c.p * chunk);  // index in the product's grouped order
+    const int s = slot - c.p * chunk;  // this XCD's slot within the product
+    const int t = deal ? (8 * (s >> 5) + x) * 32 + (s & 31) : x * chunk + s;  // index in the grouped order
     c.valid = t < mt * nt;
+    if (!c.valid) return c;  // idle slot (its group arithmetic would divide by zero)
     const int group = t / (kGroupRows * nt);
     const int first = group * kGroupRows;
     const int gsize = min(mt - first, kGroupRows);
@@ -225,7 +232,7 @@ __device__ inline void store_tile(const v4i (&acc)[8][8], int8_t *C, int ldc, in
 __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     __shared__ __attribute__((aligned(1024))) int8_t lds[kPipeBytes];
 
-    const TileCoord tc = tile_of((int)blockIdx.x, g.mt, g.nt, g.chunk);
+    const TileCoord tc = tile_of((int)blockIdx.x, g.mt, g.nt, g.chunk, g.deal);
     if (!tc.valid) return;  // whole workgroup: no barrier is pending
     const int p = tc.p, ti = tc.ti, tj = tc.tj;
 
@@ -349,7 +356,9 @@ hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
     GemmArgs ga = ga_in;
     const long tiles = (long)ga.mt * ga.nt;
     if (tiles <= 0 || ga.batch <= 0 || ga.kblocks <= 0) return hipSuccess;
-    ga.chunk = (int)((tiles + 7) / 8);
+    const long windows = (tiles + 31) / 32;
+    ga.deal = windows >= 16 ? 1 : 0;  // at least two windows per XCD
+    ga.chunk = ga.deal ? (int)(32 * ((windows + 7) / 8)) : (int)((tiles + 7) / 8);
     const long total = 8L * ga.chunk * ga.batch;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
     gemm_i8_kernel<<<(unsigned)total, kThreads, 0, st>>>(ga);

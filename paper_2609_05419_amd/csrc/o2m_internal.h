@@ -178,6 +178,7 @@ struct GemmArgs {
     int batch;
     int ldc;
     int chunk;                               // tiles per XCD per product (set by the launcher)
+    int deal;                                // 1: 32-tile windows dealt round-robin to the XCDs
     int mod[kMaxProducts];
     double inv[kMaxProducts];
 };
