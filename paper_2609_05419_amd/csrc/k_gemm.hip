@@ -63,13 +63,12 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
 // the whole chip works on one product.  Within a product the tiles follow a
 // grouped order (groups of 8 tile-rows, column-major inside a group), cut into
 // windows of 32 tiles (8 tile-rows x 4 tile-columns): the tiles resident on
-// one XCD at a time share their A and B stages in that XCD's L2.  Small
-// products give each XCD one contiguous chunk of the order.  Large ones deal
-// the windows round-robin (window w -> XCD w % 8), so that all XCDs work in
-// the same group of 8 tile-rows at once: its A strip is read once from HBM
-// and shared through the 256 MB Infinity Cache even when a product's planes
-// (2 x 256 MB at 16384^2) do not fit in it.  Slots beyond a product's tiles
-// idle.
+// one XCD at a time share their A and B stages in that XCD's L2.  Products
+// whose planes fit in the 256 MB Infinity Cache give each XCD one contiguous
+// chunk of the order.  Larger ones (2 x 256 MB at 16384^2) deal the windows
+// round-robin (window w -> XCD w % 8), so that all XCDs work in the same group
+// of 8 tile-rows at once and its A strip is read once from HBM and shared
+// through the Infinity Cache.  Slots beyond a product's tiles idle.
 struct TileCoord {
     int p, ti, tj;
     bool valid;
@@ -356,8 +355,11 @@ hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
     GemmArgs ga = ga_in;
     const long tiles = (long)ga.mt * ga.nt;
     if (tiles <= 0 || ga.batch <= 0 || ga.kblocks <= 0) return hipSuccess;
+    // deal windows when each XCD gets at least two and one product's operand
+    // planes outgrow the 256 MB Infinity Cache
     const long windows = (tiles + 31) / 32;
-    ga.deal = windows >= 16 ? 1 : 0;  // at least two windows per XCD
+    const long plane_bytes = (long)(ga.mt + ga.nt) * kStageBytes * ga.kblocks;
+    ga.deal = windows >= 16 && plane_bytes > (256L << 20) ? 1 : 0;
     ga.chunk = ga.deal ? (int)(32 * ((windows + 7) / 8)) : (int)((tiles + 7) / 8);
     const long total = 8L * ga.chunk * ga.batch;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;

@@ -359,18 +359,20 @@ def test_zherk_8192_sampled(o2m):
     assert all(C[i, i].imag == 0 for i in (0, 17, n - 1))
 
 
+@pytest.mark.slow
 def test_zgemm_dealt_windows_ragged_sampled(o2m):
-    """22 x 23 tiles of 256 (16 windows of 32, the last one partial): the int8
-    GEMM deals its tile windows to the XCDs round-robin at this size; sampled
-    entries in the first and last tile rows and columns are bit-exact."""
-    m, n, k = 22 * 256 - 37, 23 * 256 - 5, 200
+    """22 x 23 tiles of 256 (16 windows of 32, the last one partial) with
+    k = 24000, so that one product's planes outgrow the Infinity Cache and the
+    int8 GEMM deals its tile windows to the XCDs round-robin; sampled entries,
+    among them the first and last tile rows and columns, are bit-exact."""
+    m, n, k = 22 * 256 - 37, 23 * 256 - 5, 24000
     a = W.complex_matrix(m, k, 9101)
     b = W.complex_matrix(k, n, 9102)
     C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
     rng = np.random.default_rng(13)
     ent = [(0, 0), (m - 1, n - 1), (m - 1, 0), (0, n - 1), (5375, 5631), (5376, 5632)]
-    ent += [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 40), rng.integers(0, n, 40))]
-    ent += [(int(i), int(j)) for i, j in zip(rng.integers(m - 219, m, 10), rng.integers(n - 251, n, 10))]
+    ent += [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 30), rng.integers(0, n, 30))]
+    ent += [(int(i), int(j)) for i, j in zip(rng.integers(m - 219, m, 8), rng.integers(n - 251, n, 8))]
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
 
