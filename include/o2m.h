@@ -213,10 +213,14 @@ o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes);
    in *device_status and clear them. */
 o2m_status o2m_get_status(void *stream, int *device_status);
 
-/* Phase timing for profiling: when enabled, every call records HIP events
-   around its phases (scale, residues, int8 GEMM, CRT) on its stream.
-   o2m_phase_times synchronizes on the last call's events and writes the
-   elapsed milliseconds of up to max_phases phases; returns the count. */
+/* Phase timing for profiling: when enabled (which also restarts the count),
+   every call records HIP events around its phases (scale, residues, int8 GEMM,
+   CRT) on its stream, for up to 1024 calls.  o2m_phase_times waits for the
+   last timed call's events and writes, for up to max_phases phases, the
+   average elapsed milliseconds over the calls timed since enabling; it returns
+   the number of phases written (0 if no call was timed) or -1 on a HIP error
+   (for instance when a timed call on another thread has not yet recorded its
+   events).  Calls from several threads take separate event slots. */
 o2m_status o2m_phase_timing(int enable);
 int o2m_phase_times(float *ms, int max_phases);
 

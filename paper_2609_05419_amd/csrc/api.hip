@@ -8,6 +8,7 @@
 //   K3  batched int8 MFMA GEMMs, C mod m as int8       (step 4, eq. 2m-mul)
 //   K4  2M post, CRT, symmetric lift, descale          (steps 4-7, eq. 2m-post)
 // and returns without synchronizing.
+#include <atomic>
 #include <math.h>
 #include <mutex>
 #include <stdio.h>
@@ -35,8 +36,9 @@ struct DeviceState {
 std::mutex g_mu;
 DeviceState g_dev[kMaxDevices];
 
-// phase timing
-bool g_timing = false;
+// phase timing (its own lock: every call takes a slot of events)
+std::mutex g_tmu;
+std::atomic<bool> g_timing{false};
 hipEvent_t g_events[kMaxTimedCalls][kPhaseCount + 1];
 bool g_events_made[kMaxTimedCalls];
 int g_timed_calls = 0;
@@ -163,19 +165,22 @@ o2m_status workspace(size_t bytes, void **out, int **status) {
     return O2M_OK;
 }
 
-int g_call_slot = -1;
-
-void phase_mark(int phase, hipStream_t st) {
-    if (!g_timing) return;
-    if (phase == 0) {
-        if (g_timed_calls >= kMaxTimedCalls) { g_call_slot = -1; return; }
-        g_call_slot = g_timed_calls++;
-        if (!g_events_made[g_call_slot]) {
-            for (int p = 0; p <= kPhaseCount; ++p) (void)hipEventCreate(&g_events[g_call_slot][p]);
-            g_events_made[g_call_slot] = true;
-        }
+// Reserves the events of one timed call: its slot, or -1 when timing is off
+// or the table is full.
+int phase_begin() {
+    if (!g_timing.load()) return -1;
+    std::lock_guard<std::mutex> lock(g_tmu);
+    if (!g_timing.load() || g_timed_calls >= kMaxTimedCalls) return -1;
+    const int slot = g_timed_calls++;
+    if (!g_events_made[slot]) {
+        for (int p = 0; p <= kPhaseCount; ++p) (void)hipEventCreate(&g_events[slot][p]);
+        g_events_made[slot] = true;
     }
-    if (g_call_slot >= 0) (void)hipEventRecord(g_events[g_call_slot][phase], st);
+    return slot;
+}
+
+void phase_mark(int slot, int phase, hipStream_t st) {
+    if (slot >= 0) (void)hipEventRecord(g_events[slot][phase], st);
 }
 
 enum Op { kOpZ, kOpC, kOpH, kOpS, kOpG, kOpR, kOpH2, kOpS2 };
@@ -242,7 +247,8 @@ o2m_status run(const Call &c) {
 
     const ElemType et = c.op == kOpC ? kF32 : c.op == kOpG ? kI32 : is_real_split(c.op) ? kR64 : kF64;
 
-    phase_mark(0, c.st);
+    const int slot = phase_begin();
+    phase_mark(slot, 0, c.st);
     // ---- K1: maxima and exponents (rank-2k: row i of A and of B share one) --
     // maxima and sums of squares start at zero: one fill over the contiguous
     // amax_a .. ssq_b region of the workspace (carve order)
@@ -258,7 +264,7 @@ o2m_status run(const Call &c) {
         if (!sym) O2M_TRY(launch_ssq(1, et, c.k, c.n, c.B, c.ldb, b.F, b.ssq_b, c.st));
         O2M_TRY(launch_cs_exponents(c.m, b.ssq_a, b.E, sym ? 0 : c.n, b.ssq_b, b.F, c.st));
     }
-    phase_mark(1, c.st);
+    phase_mark(slot, 1, c.st);
 
     // ---- K2: residues + 2M pre ---------------------------------------------
     // Rank-2k: plane 2l = [A+ | B+], plane 2l+1 = [B- | A-] along k, so that
@@ -281,7 +287,7 @@ o2m_status run(const Call &c) {
         O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, digits(c.scaling, pB), 0,
                                 gb, t->res, b.planes_b, c.st));
     }
-    phase_mark(2, c.st);
+    phase_mark(slot, 2, c.st);
 
     // ---- K3: int8 GEMMs ----------------------------------------------------
     GemmArgs gm;
@@ -304,7 +310,7 @@ o2m_status run(const Call &c) {
         gm.inv[p] = t->res.inv[l];
     }
     O2M_TRY(launch_gemm(gm, c.st));
-    phase_mark(3, c.st);
+    phase_mark(slot, 3, c.st);
 
     // ---- K4: 2M post + CRT + lift + descale ---------------------------------
     CrtArgs ca;
@@ -342,7 +348,7 @@ o2m_status run(const Call &c) {
         if (c.E_out) O2M_TRY(hipMemcpyAsync(c.E_out, b.E, sizeof(int32_t) * c.m, hipMemcpyDeviceToDevice, c.st));
         if (c.F_out) O2M_TRY(hipMemcpyAsync(c.F_out, b.F, sizeof(int32_t) * c.n, hipMemcpyDeviceToDevice, c.st));
     }
-    phase_mark(4, c.st);
+    phase_mark(slot, 4, c.st);
     if (getenv("O2M_LOG"))
         fprintf(stderr, "o2m: op=%d m=%d n=%d k=%d N=%d scaling=%d log2M=%.2f pA=%d pB=%d T=%d ws=%zu\n",
                 (int)c.op, c.m, c.n, c.k, c.N, c.scaling, t->log2M, pA, pB, t->crt.limbs, need);
@@ -588,13 +594,15 @@ o2m_status o2m_get_status(void *stream, int *device_status) {
 }
 
 o2m_status o2m_phase_timing(int enable) {
-    g_timing = enable != 0;
+    std::lock_guard<std::mutex> lock(g_tmu);
+    g_timing.store(enable != 0);
     g_timed_calls = 0;
-    g_call_slot = -1;
     return O2M_OK;
 }
 
 int o2m_phase_times(float *ms, int max_phases) {
+    if (!ms || max_phases < 0) return -1;
+    std::lock_guard<std::mutex> lock(g_tmu);
     const int n = g_timed_calls;
     int count = kPhaseCount < max_phases ? kPhaseCount : max_phases;
     for (int p = 0; p < count; ++p) ms[p] = 0.0f;

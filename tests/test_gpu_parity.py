@@ -461,6 +461,29 @@ def test_calls_on_a_side_stream(o2m):
     assert same_bits(np.asfortranarray(C2.cpu().numpy()), O.oq_zgemm(a, b, 12))
 
 
+def test_phase_timing(o2m):
+    """The per-phase HIP events: four positive phase times averaged over the
+    calls since enabling, a restart on re-enabling, nothing while disabled,
+    and results unchanged by the timing."""
+    a = W.complex_matrix(300, 200, 441)
+    b = W.complex_matrix(200, 260, 442)
+    A, B = to_dev(a), to_dev(b)
+    o2m.phase_timing(True)
+    try:
+        for _ in range(3):
+            C = o2m.zgemm_2m(A, B, n_moduli=16)
+        t = o2m.phase_times()
+        assert list(t) == ["scale", "residues", "int8_gemm", "crt"]
+        assert all(v > 0.0 for v in t.values()), t
+        o2m.phase_timing(True)                      # restart: no call timed yet
+        assert o2m.phase_times() == {}
+    finally:
+        o2m.phase_timing(False)
+    o2m.zgemm_2m(A, B, n_moduli=16)
+    assert o2m.phase_times() == {}
+    assert same_bits(host(C), O.oq_zgemm(a, b, 16))
+
+
 @pytest.mark.slow
 def test_zgemm_k_at_the_int32_limit_sampled(o2m):
     """k = 149130, the largest k whose int32 accumulation is exact with 2M
