@@ -96,6 +96,7 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halve
 
 struct Buffers {
     unsigned long long *amax_a, *amax_b, *ssq_a, *ssq_b;
+    unsigned *queue;  // the int8 GEMM's slot counters
     int32_t *E, *F;
     int8_t *planes_a, *planes_b, *res;
 };
@@ -103,12 +104,13 @@ struct Buffers {
 size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
     Carver c(base);
     Buffers t;
-    // amax_a, amax_b, ssq_a, ssq_b stay contiguous and in this order, ending
-    // where E begins: K1 clears them with one fill
+    // amax_a, amax_b, ssq_a, ssq_b and queue stay contiguous and in this
+    // order, ending where E begins: K1 clears them with one fill
     t.amax_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
     t.amax_b = g.shared_planes ? t.amax_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
     t.ssq_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
     t.ssq_b = g.shared_planes ? t.ssq_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
+    t.queue = (unsigned *)c.take(sizeof(unsigned) * 8 * kQueueStride);
     t.E = (int32_t *)c.take(sizeof(int32_t) * g.a_pad);
     t.F = g.shared_planes ? t.E : (int32_t *)c.take(sizeof(int32_t) * g.b_pad);
     t.planes_a = (int8_t *)c.take(g.plane_a * g.planes);
@@ -250,8 +252,9 @@ o2m_status run(const Call &c) {
     const int slot = phase_begin();
     phase_mark(slot, 0, c.st);
     // ---- K1: maxima and exponents (rank-2k: row i of A and of B share one) --
-    // maxima and sums of squares start at zero: one fill over the contiguous
-    // amax_a .. ssq_b region of the workspace (carve order)
+    // maxima, sums of squares and the GEMM's slot counters start at zero: one
+    // fill over the contiguous amax_a .. queue region of the workspace (carve
+    // order)
     O2M_TRY(launch_zero(b.amax_a, (size_t)((char *)b.E - (char *)b.amax_a), c.st));
     O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
     if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
@@ -295,6 +298,7 @@ o2m_status run(const Call &c) {
     gm.a = b.planes_a;
     gm.b = sym ? b.planes_a + g.plane_a : b.planes_b;
     gm.c = b.res;
+    gm.queue = b.queue;
     gm.a_pstride = sym ? 2 * g.plane_a : g.plane_a;
     gm.b_pstride = sym ? 2 * g.plane_a : g.plane_b;
     gm.c_pstride = g.plane_c;

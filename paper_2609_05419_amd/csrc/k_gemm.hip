@@ -57,27 +57,26 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
     return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
 }
 
-// Tile schedule.  The hardware deals workgroups to the 8 XCDs round-robin
-// (workgroup b -> XCD b % 8, in dispatch order b / 8 within it), and all XCDs
-// sweep the batch items (one int8 GEMM each) in the same order, so at any time
-// the whole chip works on one product.  Within a product the tiles follow a
-// grouped order (groups of 8 tile-rows, column-major inside a group), cut into
-// windows of 32 tiles (8 tile-rows x 4 tile-columns): the tiles resident on
-// one XCD at a time share their A and B stages in that XCD's L2.  Products
-// whose planes fit in the 256 MB Infinity Cache give each XCD one contiguous
-// chunk of the order.  Larger ones (2 x 256 MB at 16384^2) deal the windows
-// round-robin (window w -> XCD w % 8), so that all XCDs work in the same group
-// of 8 tile-rows at once and its A strip is read once from HBM and shared
-// through the Infinity Cache.  Slots beyond a product's tiles idle.
+// Tile schedule.  Each XCD has a queue of slots, and within a product the
+// slots follow a grouped order of the tiles (groups of 8 tile-rows,
+// column-major inside a group), cut into windows of 32 tiles (8 tile-rows x
+// 4 tile-columns): the tiles resident on one XCD at a time share their A and
+// B stages in that XCD's L2.  All XCDs sweep the batch items (one int8 GEMM
+// each) in the same order, so at any time the whole chip works on one
+// product.  Products whose planes fit in the 256 MB Infinity Cache give each
+// XCD one contiguous chunk of the order.  Larger ones (2 x 256 MB at 16384^2)
+// deal the windows round-robin (window w -> XCD w % 8), so that all XCDs work
+// in the same group of 8 tile-rows at once and its A strip is read once from
+// HBM and shared through the Infinity Cache.  Slots beyond a product's tiles
+// idle.
 struct TileCoord {
     int p, ti, tj;
     bool valid;
 };
-__device__ inline TileCoord tile_of(int b, int mt, int nt, int chunk, int deal) {
+__device__ inline TileCoord tile_of(int x, int slot, int mt, int nt, int chunk, int deal) {
     TileCoord c;
-    const int x = b & 7, slot = b >> 3;
     c.p = slot / chunk;
-    const int s = slot - c.p * chunk;  // this XCD's slot within the product
+    const int s = slot - c.p * chunk;  // the slot within the product
     const int t = deal ? (8 * (s >> 5) + x) * 32 + (s & 31) : x * chunk + s;  // index in the grouped order
     c.valid = t < mt * nt;
     if (!c.valid) return c;  // idle slot (its group arithmetic would divide by zero)
@@ -88,6 +87,45 @@ __device__ inline TileCoord tile_of(int b, int mt, int nt, int chunk, int deal) 
     c.ti = first + within % gsize;
     c.tj = within / gsize;
     return c;
+}
+
+// The XCDs of the part do not run at one clock (up to a tenth apart under
+// this load), so a fixed share of tiles per XCD would leave the fast ones idle
+// while the slowest finishes.  Workgroups therefore claim slots at run time:
+// wave 0 takes the next slot of its own XCD's queue (the hardware XCC_ID
+// register names the XCD), and once that queue is empty, the next slot of the
+// first other queue that still has one.  The launch carries spare workgroups
+// for those extra claims; a workgroup that finds every queue empty exits.
+// Each claimed slot is handed out once (atomic counters, which start at zero),
+// and every slot is claimed: a workgroup only finds all queues empty when all
+// slots are taken, and there are more workgroups than slots.
+constexpr int kHwRegXccId = (31 << 11) | 20;  // s_getreg operand: all 32 bits of XCC_ID
+
+__device__ inline unsigned claim_next(unsigned *q) {
+    return __hip_atomic_fetch_add(q, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Run by all lanes of one wave; returns x << 28 | slot, or -1 (wave-uniform).
+__device__ inline int claim_slot(unsigned *queue, unsigned slots, int lane) {
+    const int x = __builtin_amdgcn_s_getreg(kHwRegXccId) & 7;
+    unsigned t = lane == 0 ? claim_next(queue + x * kQueueStride) : 0u;
+    t = __builtin_amdgcn_readfirstlane(t);
+    if (t < slots) return (x << 28) | (int)t;
+    // own queue empty: look at the others all at once, then claim in turn
+    const int y = (x + lane) & 7;
+    const unsigned used =
+        lane >= 1 && lane < 8 ? __hip_atomic_load(queue + y * kQueueStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                              : slots;
+    unsigned long long open = __ballot(used < slots);
+    while (open) {
+        const int i = __builtin_ctzll(open);
+        open &= open - 1;
+        const int z = (x + i) & 7;
+        t = lane == 0 ? claim_next(queue + z * kQueueStride) : 0u;
+        t = __builtin_amdgcn_readfirstlane(t);
+        if (t < slots) return (z << 28) | (int)t;
+    }
+    return -1;
 }
 
 // s_waitcnt on the vector-memory counter only (gfx9 encoding), n <= 63
@@ -228,34 +266,40 @@ __device__ inline void store_tile(const v4i (&acc)[8][8], int8_t *C, int ldc, in
     }
 }
 
-__global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
-    __shared__ __attribute__((aligned(1024))) int8_t lds[kPipeBytes];
+// One wave's place in the workgroup's pipeline.
+struct Wave {
+    int8_t *lds;     // the ring of kStages stage buffers
+    int tid, lane;
+    int wave;        // wave-uniform
+    int aoff, boff;  // this wave's A and B fragments within a stage buffer
+};
 
-    const TileCoord tc = tile_of((int)blockIdx.x, g.mt, g.nt, g.chunk, g.deal);
-    if (!tc.valid) return;  // whole workgroup: no barrier is pending
-    const int p = tc.p, ti = tc.ti, tj = tc.tj;
+__device__ inline Wave wave_of(int8_t *lds) {
+    Wave w;
+    w.lds = lds;
+    w.tid = threadIdx.x;
+    w.lane = w.tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(w.tid >> 6);  // wave-uniform (SGPR)
+    const int wr = w.wave >> 1, wc = w.wave & 1;          // 2 x 2 waves of 128 x 128
+    w.aoff = wr * 8 * kFragBytes;
+    w.boff = kStageBytes + wc * 8 * kFragBytes;
+    return w;
+}
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
-    const int wr = wave >> 1, wc = wave & 1;                     // 2 x 2 waves of 128 x 128
-    const int KB = g.kblocks;
-    const int aoff = wr * 8 * kFragBytes, boff = kStageBytes + wc * 8 * kFragBytes;
-
-    const __amdgpu_buffer_rsrc_t rA = tile_rsrc(g.a + (size_t)p * g.a_pstride + (size_t)ti * KB * kStageBytes, KB);
-    const __amdgpu_buffer_rsrc_t rB = tile_rsrc(g.b + (size_t)p * g.b_pstride + (size_t)tj * KB * kStageBytes, KB);
-
-    v4i acc[8][8];
+__device__ inline void zero_acc(v4i (&acc)[8][8]) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = v4i{};
     acc_after_fill(acc);
+}
 
-    // prologue: fill the ring, then wait for stage 0
+// Fill the ring with the first min(KB, kStages) stages of one tile, wait for
+// stage 0 and read its fragments into (fa, fb).
+__device__ inline void prologue(const Wave &w, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB, int KB,
+                                v4i (&fa)[8], v4i (&fb)[8]) {
     const int pre = KB < kStages ? KB : kStages;
-    for (int s = 0; s < pre; ++s)
-        load_stage(rA, rB, s, lds + s * kStageBuf, tid, wave);
+    for (int s = 0; s < pre; ++s) load_stage(rA, rB, s, w.lds + s * kStageBuf, w.tid, w.wave);
     switch (pre) {
     case 1: wait_vm<0>(); break;
     case 2: wait_vm<kLoadsPerStage>(); break;
@@ -263,76 +307,126 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     default: wait_vm<3 * kLoadsPerStage>(); break;
     }
     stage_barrier();
-
-    // Fragments of the current stage (f0 = A, g0 = B) and of the next one.
-    v4i fa0[8], fb0[8], fa1[8], fb1[8];
 #pragma unroll
     for (int f = 0; f < 8; ++f) {
-        fa0[f] = read_frag(lds, aoff, boff, lane, f);
-        fb0[f] = read_frag(lds, aoff, boff, lane, 8 + f);
+        fa[f] = read_frag(w.lds, w.aoff, w.boff, w.lane, f);
+        fb[f] = read_frag(w.lds, w.aoff, w.boff, w.lane, 8 + f);
     }
     wait_lds();
+}
 
-    // Stage kb, its fragments in (ca, cb): wait until stage kb+1 has landed
-    // (`younger` later stages may stay in flight), barrier (every wave is done
-    // reading stage kb, so its buffer is free), then the 64 MFMAs of stage kb
-    // with the fragment reads of stage kb+1 into (na, nb) and the copy of stage
-    // kb+4 into the freed buffer.  In the steady state they are interleaved
-    // with the MFMAs; the last stages issue them first.
-    auto stage = [&](int kb, v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8], int younger, bool next,
-                     bool refill) {
-        if (younger >= 2) wait_vm<2 * kLoadsPerStage>();
-        else if (younger == 1) wait_vm<kLoadsPerStage>();
-        else wait_vm<0>();
-        stage_barrier();
-        const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
-        if (next) {
+// Stage kb, its fragments in (ca, cb): wait until stage kb+1 has landed
+// (`younger` later stages may stay in flight), barrier (every wave is done
+// reading stage kb, so its buffer is free), then the 64 MFMAs of stage kb with
+// the fragment reads of stage kb+1 into (na, nb) and, if `refill`, the copy of
+// stage kb+4 of (rA, rB) into the freed buffer, both issued first.  Used for
+// the last stages of a tile, where waits shrink.
+__device__ inline void edge_stage(v4i (&acc)[8][8], const Wave &w, int kb, const v4i (&ca)[8], const v4i (&cb)[8],
+                                  v4i (&na)[8], v4i (&nb)[8], int younger, bool next, bool refill,
+                                  __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB) {
+    if (younger >= 2) wait_vm<2 * kLoadsPerStage>();
+    else if (younger == 1) wait_vm<kLoadsPerStage>();
+    else wait_vm<0>();
+    stage_barrier();
+    const int8_t *nbuf = w.lds + ((kb + 1) % kStages) * kStageBuf;
+    if (next) {
 #pragma unroll
-            for (int f = 0; f < 8; ++f) {
-                na[f] = read_frag(nbuf, aoff, boff, lane, f);
-                nb[f] = read_frag(nbuf, aoff, boff, lane, 8 + f);
-            }
+        for (int f = 0; f < 8; ++f) {
+            na[f] = read_frag(nbuf, w.aoff, w.boff, w.lane, f);
+            nb[f] = read_frag(nbuf, w.aoff, w.boff, w.lane, 8 + f);
         }
-        if (refill) load_stage(rA, rB, kb + kStages, lds + (kb % kStages) * kStageBuf, tid, wave);
+    }
+    if (refill) load_stage(rA, rB, kb + kStages, w.lds + (kb % kStages) * kStageBuf, w.tid, w.wave);
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) mfma(acc[i][j], ca[i], cb[j]);
-        wait_lds();  // the next stage's fragments are in registers
-    };
-    auto steady = [&](int kb, v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8]) {
-        wait_vm<2 * kLoadsPerStage>();
-        stage_barrier();
-        const int8_t *nbuf = lds + ((kb + 1) % kStages) * kStageBuf;
-        int8_t *rbuf = lds + (kb % kStages) * kStageBuf;
+        for (int j = 0; j < 8; ++j) mfma(acc[i][j], ca[i], cb[j]);
+    wait_lds();  // the next stage's fragments are in registers
+}
+
+// Steady-state stage kb: as edge_stage with two younger stages in flight, but
+// the fragment reads of stage kb+1 follow every other one of the first 32
+// MFMAs and the 8 copies of stage `sstage` (= kb+4) of (sA, sB) into the
+// freed buffer every fourth one of the last 32.
+__device__ inline void steady_stage(v4i (&acc)[8][8], const Wave &w, int kb, const v4i (&ca)[8], const v4i (&cb)[8],
+                                    v4i (&na)[8], v4i (&nb)[8], __amdgpu_buffer_rsrc_t sA,
+                                    __amdgpu_buffer_rsrc_t sB, int sstage) {
+    wait_vm<2 * kLoadsPerStage>();
+    stage_barrier();
+    const int8_t *nbuf = w.lds + ((kb + 1) % kStages) * kStageBuf;
+    int8_t *rbuf = w.lds + (kb % kStages) * kStageBuf;
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                mfma(acc[i][j], ca[i], cb[j]);
-                const int t = 8 * i + j;
-                // fragment reads after every other MFMA of the first half, the
-                // stage copy after every fourth of the second half
-                if (t < 32 && (t & 1) == 0) {
-                    const int f = t >> 1;
-                    if (f < 8) na[f] = read_frag(nbuf, aoff, boff, lane, f);
-                    else nb[f - 8] = read_frag(nbuf, aoff, boff, lane, f);
-                }
-                if (t >= 32 && (t & 3) == 0) load_part(rA, rB, kb + kStages, rbuf, tid, wave, (t - 32) >> 2);
+        for (int j = 0; j < 8; ++j) {
+            mfma(acc[i][j], ca[i], cb[j]);
+            const int t = 8 * i + j;
+            if (t < 32 && (t & 1) == 0) {
+                const int f = t >> 1;
+                if (f < 8) na[f] = read_frag(nbuf, w.aoff, w.boff, w.lane, f);
+                else nb[f - 8] = read_frag(nbuf, w.aoff, w.boff, w.lane, f);
             }
-        wait_lds();
-    };
+            if (t >= 32 && (t & 3) == 0) load_part(sA, sB, sstage, rbuf, w.tid, w.wave, (t - 32) >> 2);
+        }
+    wait_lds();
+}
+
+// The tile's output block for this wave: C mod m as int8.
+__device__ inline void epilogue(v4i (&acc)[8][8], const Wave &w, const GemmArgs &g, const TileCoord &tc) {
+    acc_after_mfma(acc);
+    const int wr = w.wave >> 1, wc = w.wave & 1;
+    int8_t *C = g.c + (size_t)tc.p * g.c_pstride + (size_t)(tc.tj * 256 + wc * 128 + (w.lane & 15)) * g.ldc +
+                tc.ti * 256 + wr * 128 + 16 * (w.lane >> 4);
+    store_tile(acc, C, g.ldc, g.mod[tc.p], g.inv[tc.p]);
+}
+
+__device__ inline __amdgpu_buffer_rsrc_t rsrc_a(const GemmArgs &g, const TileCoord &tc) {
+    return tile_rsrc(g.a + (size_t)tc.p * g.a_pstride + (size_t)tc.ti * g.kblocks * kStageBytes, g.kblocks);
+}
+__device__ inline __amdgpu_buffer_rsrc_t rsrc_b(const GemmArgs &g, const TileCoord &tc) {
+    return tile_rsrc(g.b + (size_t)tc.p * g.b_pstride + (size_t)tc.tj * g.kblocks * kStageBytes, g.kblocks);
+}
+
+// One output tile per workgroup, claimed at start.
+__global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
+    // One LDS object: the stage ring and, past its end, the claimed slot.  A
+    // second __shared__ variable would give the compiler alias scopes for LDS,
+    // with which it waits for every stage copy in flight (vmcnt(0)) before
+    // each fragment read of the k-loop.
+    __shared__ __attribute__((aligned(1024))) int8_t lds[kPipeBytes + 16];
+    int *claimed = reinterpret_cast<int *>(lds + kPipeBytes);
+
+    const Wave w = wave_of(lds);
+    if (w.wave == 0) {
+        const int c = claim_slot(g.queue, (unsigned)(g.chunk * g.batch), w.lane);
+        if (w.lane == 0) *claimed = c;
+    }
+    v4i acc[8][8];
+    zero_acc(acc);  // while the claim is in flight
+    __syncthreads();
+    const int c = *claimed;
+    if (c < 0) return;  // whole workgroup: no barrier is pending
+    const TileCoord tc = tile_of(c >> 28, c & 0x0FFFFFFF, g.mt, g.nt, g.chunk, g.deal);
+    if (!tc.valid) return;
+    const int KB = g.kblocks;
+    const __amdgpu_buffer_rsrc_t rA = rsrc_a(g, tc), rB = rsrc_b(g, tc);
+
+    // Fragments of the current stage (fa0, fb0) and of the next one.
+    v4i fa0[8], fb0[8], fa1[8], fb1[8];
+    prologue(w, rA, rB, KB, fa0, fb0);
+
     // Steady state, two stages per trip so that the fragment sets alternate
     // statically; then at most five stages with shrinking waits, the sets
     // still alternating statically.
     int kb = 0;
     for (; kb + kStages + 1 < KB; kb += 2) {
-        steady(kb, fa0, fb0, fa1, fb1);
-        steady(kb + 1, fa1, fb1, fa0, fb0);
+        steady_stage(acc, w, kb, fa0, fb0, fa1, fb1, rA, rB, kb + kStages);
+        steady_stage(acc, w, kb + 1, fa1, fb1, fa0, fb0, rA, rB, kb + 1 + kStages);
     }
     auto tail = [&](v4i (&ca)[8], v4i (&cb)[8], v4i (&na)[8], v4i (&nb)[8]) {
         if (kb < KB) {
-            stage(kb, ca, cb, na, nb, min(KB - 1, kb + kStages - 1) - (kb + 1), kb + 1 < KB, kb + kStages < KB);
+            edge_stage(acc, w, kb, ca, cb, na, nb, min(KB - 1, kb + kStages - 1) - (kb + 1), kb + 1 < KB,
+                       kb + kStages < KB, rA, rB);
             ++kb;
         }
     };
@@ -342,10 +436,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     tail(fa1, fb1, fa0, fb0);
     tail(fa0, fb0, fa1, fb1);
 
-    acc_after_mfma(acc);
-    int8_t *C = g.c + (size_t)p * g.c_pstride + (size_t)(tj * 256 + wc * 128 + (lane & 15)) * g.ldc + ti * 256 +
-                wr * 128 + 16 * (lane >> 4);
-    store_tile(acc, C, g.ldc, g.mod[p], g.inv[p]);
+    epilogue(acc, w, g, tc);
 }
 
 }  // namespace
@@ -363,7 +454,11 @@ hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
     ga.chunk = ga.deal ? (int)(32 * ((windows + 7) / 8)) : (int)((tiles + 7) / 8);
     const long total = 8L * ga.chunk * ga.batch;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-    gemm_i8_kernel<<<(unsigned)total, kThreads, 0, st>>>(ga);
+    // one spare workgroup per 16 slots of each XCD: a faster XCD takes tiles
+    // of a slower one's queue once its own is empty
+    const long grid = total + 8 * ((ga.chunk * (long)ga.batch + 15) / 16);
+    if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+    gemm_i8_kernel<<<(unsigned)grid, kThreads, 0, st>>>(ga);
     return hipGetLastError();
 }
 

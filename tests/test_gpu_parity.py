@@ -378,6 +378,28 @@ def test_zgemm_dealt_windows_ragged_sampled(o2m):
     assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
 
 
+CLAIMED = [
+    # m, n, k, N: many tiles per product and more workgroups than slots, so
+    # that the int8 GEMM's workgroups claim tiles from the per-XCD queues and
+    # take over other queues' slots once their own is empty.  k = 250: one
+    # ring of 4 k-stages per tile; N = 22: 44 products of 16 tiles each.
+    (8 * 256 - 13, 4 * 256 - 7, 250, 16),
+    (4 * 256 - 13, 4 * 256 - 7, 500, 22),
+]
+
+
+@pytest.mark.parametrize("case", CLAIMED, ids=[f"{c[0]}x{c[1]}x{c[2]}-N{c[3]}" for c in CLAIMED])
+def test_zgemm_claimed_tiles_bit_exact(o2m, case):
+    """Whole outputs bit-exact against the oracle: every tile of every
+    product computed exactly once whichever workgroup claims it."""
+    m, n, k, N = case
+    a = W.complex_matrix(m, k, 9201 + N, dist="phi", phi=2.0)
+    b = W.complex_matrix(k, n, 9202 + N, dist="phi", phi=2.0)
+    print(f"[parity] claimed tiles {m}x{n}x{k} N={N}", flush=True)
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N))
+    assert same_bits(got, O.oq_zgemm(a, b, N))
+
+
 @pytest.mark.slow
 def test_zgemm_tall_skinny_sampled(o2m):
     """m = n = 4096, k = 65536 (N = 16): int32 headroom and the long k-loop."""
