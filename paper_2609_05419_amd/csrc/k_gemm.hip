@@ -91,14 +91,20 @@ __device__ inline TileCoord tile_of(int x, int slot, int mt, int nt, int chunk, 
 
 // The XCDs of the part do not run at one clock (up to a tenth apart under
 // this load), so a fixed share of tiles per XCD would leave the fast ones idle
-// while the slowest finishes.  Workgroups therefore claim slots at run time:
-// wave 0 takes the next slot of its own XCD's queue (the hardware XCC_ID
-// register names the XCD), and once that queue is empty, the next slot of the
-// first other queue that still has one.  The launch carries spare workgroups
-// for those extra claims; a workgroup that finds every queue empty exits.
-// Each claimed slot is handed out once (atomic counters, which start at zero),
-// and every slot is claimed: a workgroup only finds all queues empty when all
-// slots are taken, and there are more workgroups than slots.
+// while the slowest finishes.  The first 7/8 of each XCD's slots therefore go
+// to workgroups by index, as dispatched (workgroup b runs on XCD b % 8 and
+// takes its slot b / 8), and the last 1/8 form a pool that workgroups claim
+// at run time: the next slot of the pool of their own XCD (the hardware
+// XCC_ID register names it), and once that is empty, the next slot of the
+// first other pool that still has one.  The launch carries spare workgroups
+// for those extra claims; a workgroup that finds every pool empty exits.
+// Only the pool's workgroups wait for an atomic round trip before their first
+// stage copy, and the spares cost a few microseconds at the end, so short
+// launches (fewer than 128 k-stages or 256 slots per XCD, where that cost
+// outweighs the balance) keep every slot fixed.  Each pool slot is handed out once (atomic counters, which
+// start at zero), and every one is claimed: a workgroup only finds all pools
+// empty when all their slots are taken, and the pools have more workgroups
+// than slots.
 constexpr int kHwRegXccId = (31 << 11) | 20;  // s_getreg operand: all 32 bits of XCC_ID
 
 __device__ inline unsigned claim_next(unsigned *q) {
@@ -106,24 +112,25 @@ __device__ inline unsigned claim_next(unsigned *q) {
 }
 
 // Run by all lanes of one wave; returns x << 28 | slot, or -1 (wave-uniform).
-__device__ inline int claim_slot(unsigned *queue, unsigned slots, int lane) {
+// Pool x holds slots [S, slots) of XCD x; its counter counts the claims.
+__device__ inline int claim_slot(unsigned *queue, unsigned S, unsigned slots, int lane) {
     const int x = __builtin_amdgcn_s_getreg(kHwRegXccId) & 7;
     unsigned t = lane == 0 ? claim_next(queue + x * kQueueStride) : 0u;
     t = __builtin_amdgcn_readfirstlane(t);
-    if (t < slots) return (x << 28) | (int)t;
-    // own queue empty: look at the others all at once, then claim in turn
+    if (t < slots - S) return (x << 28) | (int)(S + t);
+    // own pool empty: look at the others all at once, then claim in turn
     const int y = (x + lane) & 7;
     const unsigned used =
         lane >= 1 && lane < 8 ? __hip_atomic_load(queue + y * kQueueStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                               : slots;
-    unsigned long long open = __ballot(used < slots);
+    unsigned long long open = __ballot(used < slots - S);
     while (open) {
         const int i = __builtin_ctzll(open);
         open &= open - 1;
         const int z = (x + i) & 7;
         t = lane == 0 ? claim_next(queue + z * kQueueStride) : 0u;
         t = __builtin_amdgcn_readfirstlane(t);
-        if (t < slots) return (z << 28) | (int)t;
+        if (t < slots - S) return (z << 28) | (int)(S + t);
     }
     return -1;
 }
@@ -387,7 +394,7 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc_b(const GemmArgs &g, const TileCoo
     return tile_rsrc(g.b + (size_t)tc.p * g.b_pstride + (size_t)tc.tj * g.kblocks * kStageBytes, g.kblocks);
 }
 
-// One output tile per workgroup, claimed at start.
+// One output tile per workgroup.
 __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     // One LDS object: the stage ring and, past its end, the claimed slot.  A
     // second __shared__ variable would give the compiler alias scopes for LDS,
@@ -397,19 +404,33 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
     int *claimed = reinterpret_cast<int *>(lds + kPipeBytes);
 
     const Wave w = wave_of(lds);
-    if (w.wave == 0) {
-        const int c = claim_slot(g.queue, (unsigned)(g.chunk * g.batch), w.lane);
-        if (w.lane == 0) *claimed = c;
-    }
+    const int slots = g.chunk * g.batch;  // per XCD
     v4i acc[8][8];
-    zero_acc(acc);  // while the claim is in flight
-    __syncthreads();
-    const int c = *claimed;
-    if (c < 0) return;  // whole workgroup: no barrier is pending
-    const TileCoord tc = tile_of(c >> 28, c & 0x0FFFFFFF, g.mt, g.nt, g.chunk, g.deal);
-    if (!tc.valid) return;
+    TileCoord tc;
+    __amdgpu_buffer_rsrc_t rA, rB;
+    if ((int)(blockIdx.x >> 3) < g.fixed) {
+        // the tile and its operands are worked out before the accumulator fill,
+        // so that the argument loads they need are not waited for behind it
+        tc = tile_of(blockIdx.x & 7, blockIdx.x >> 3, g.mt, g.nt, g.chunk, g.deal);
+        if (!tc.valid) return;  // whole workgroup: no barrier is pending
+        rA = rsrc_a(g, tc);
+        rB = rsrc_b(g, tc);
+        zero_acc(acc);
+    } else {
+        if (w.wave == 0) {
+            const int r = claim_slot(g.queue, (unsigned)g.fixed, (unsigned)slots, w.lane);
+            if (w.lane == 0) *claimed = r;
+        }
+        zero_acc(acc);  // while the claim is in flight
+        __syncthreads();
+        const int c = *claimed;
+        if (c < 0) return;  // whole workgroup: no barrier is pending
+        tc = tile_of(c >> 28, c & 0x0FFFFFFF, g.mt, g.nt, g.chunk, g.deal);
+        if (!tc.valid) return;
+        rA = rsrc_a(g, tc);
+        rB = rsrc_b(g, tc);
+    }
     const int KB = g.kblocks;
-    const __amdgpu_buffer_rsrc_t rA = rsrc_a(g, tc), rB = rsrc_b(g, tc);
 
     // Fragments of the current stage (fa0, fb0) and of the next one.
     v4i fa0[8], fb0[8], fa1[8], fb1[8];
@@ -454,9 +475,12 @@ hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
     ga.chunk = ga.deal ? (int)(32 * ((windows + 7) / 8)) : (int)((tiles + 7) / 8);
     const long total = 8L * ga.chunk * ga.batch;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-    // one spare workgroup per 16 slots of each XCD: a faster XCD takes tiles
-    // of a slower one's queue once its own is empty
-    const long grid = total + 8 * ((ga.chunk * (long)ga.batch + 15) / 16);
+    // pooled: the last 1/8 of each XCD's slots, plus one spare workgroup per
+    // 12 slots, so that a faster XCD can take slots of a slower one's pool
+    const long slots = ga.chunk * (long)ga.batch;
+    const bool pool = ga.kblocks >= 128 && slots >= 256;
+    ga.fixed = (int)(pool ? slots - slots / 8 : slots);
+    const long grid = total + (pool ? 8 * ((slots + 11) / 12) : 0);
     if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
     gemm_i8_kernel<<<(unsigned)grid, kThreads, 0, st>>>(ga);
     return hipGetLastError();

@@ -169,7 +169,7 @@ inline int residue_digits(int bits) {
 // C_p mod m_p stored as int8 (symmetric residue), column-major with leading
 // dimension ldc = m_pad, plane stride ldc * n_pad.  mod[p], inv[p]: the
 // modulus of product p and its fp64 reciprocal.
-// The int8 GEMM's slot counters sit kQueueStride unsigned apart (256 bytes):
+// The int8 GEMM's pool counters sit kQueueStride unsigned apart (256 bytes):
 // one cache line each, so that claims on different queues do not serialize.
 constexpr int kQueueStride = 64;
 
@@ -183,7 +183,8 @@ struct GemmArgs {
     int ldc;
     int chunk;                               // tiles per XCD per product (set by the launcher)
     int deal;                                // 1: 32-tile windows dealt round-robin to the XCDs
-    unsigned *queue;                         // 8 slot counters, one per XCD, kQueueStride
+    int fixed;                               // slots per XCD taken by workgroup index (launcher)
+    unsigned *queue;                         // 8 pool counters, one per XCD, kQueueStride
                                              // apart; zero at launch
     int mod[kMaxProducts];
     double inv[kMaxProducts];

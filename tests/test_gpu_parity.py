@@ -378,26 +378,46 @@ def test_zgemm_dealt_windows_ragged_sampled(o2m):
     assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
 
 
-CLAIMED = [
-    # m, n, k, N: many tiles per product and more workgroups than slots, so
-    # that the int8 GEMM's workgroups claim tiles from the per-XCD queues and
-    # take over other queues' slots once their own is empty.  k = 250: one
-    # ring of 4 k-stages per tile; N = 22: 44 products of 16 tiles each.
+MANY_TILES = [
+    # m, n, k, N: many tiles per product, ragged edges; k = 250: one ring of 4
+    # k-stages per tile; N = 22: 44 products of 16 tiles each.
     (8 * 256 - 13, 4 * 256 - 7, 250, 16),
     (4 * 256 - 13, 4 * 256 - 7, 500, 22),
 ]
 
 
-@pytest.mark.parametrize("case", CLAIMED, ids=[f"{c[0]}x{c[1]}x{c[2]}-N{c[3]}" for c in CLAIMED])
-def test_zgemm_claimed_tiles_bit_exact(o2m, case):
-    """Whole outputs bit-exact against the oracle: every tile of every
-    product computed exactly once whichever workgroup claims it."""
+@pytest.mark.parametrize("case", MANY_TILES, ids=[f"{c[0]}x{c[1]}x{c[2]}-N{c[3]}" for c in MANY_TILES])
+def test_zgemm_many_tiles_bit_exact(o2m, case):
+    """Whole outputs bit-exact against the oracle over many output tiles."""
     m, n, k, N = case
     a = W.complex_matrix(m, k, 9201 + N, dist="phi", phi=2.0)
     b = W.complex_matrix(k, n, 9202 + N, dist="phi", phi=2.0)
-    print(f"[parity] claimed tiles {m}x{n}x{k} N={N}", flush=True)
+    print(f"[parity] many tiles {m}x{n}x{k} N={N}", flush=True)
     got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N))
     assert same_bits(got, O.oq_zgemm(a, b, N))
+
+
+def test_zgemm_pooled_tiles_sampled(o2m):
+    """129 k-stages and 8 x 8 tiles per product, 32 products: 256 slots per
+    XCD, so the int8 GEMM leaves the last eighth of every XCD's slots to a
+    pool that workgroups claim at run time (with spares that take slots of
+    other XCDs' pools).  Two sampled entries in every 256 x 256 output tile,
+    each depending on that tile of all 32 products, are bit-exact: a tile
+    skipped or computed twice by the claims would show."""
+    m, n, k = 8 * 256 - 21, 8 * 256 - 3, 8200
+    a = W.complex_matrix(m, k, 9301)
+    b = W.complex_matrix(k, n, 9302)
+    print(f"[parity] pooled tiles {m}x{n}x{k} N=16", flush=True)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    rng = np.random.default_rng(31)
+    ent = [(m - 1, n - 1)]
+    for ti in range(8):
+        for tj in range(8):
+            hi_i, hi_j = min(256, m - 256 * ti), min(256, n - 256 * tj)
+            for _ in range(2):
+                ent.append((256 * ti + int(rng.integers(0, hi_i)), 256 * tj + int(rng.integers(0, hi_j))))
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
 
 
 @pytest.mark.slow
