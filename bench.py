@@ -38,7 +38,7 @@ def log(*a):
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("k_gemm.hip", "o2m_internal.h"):
+    for f in ("k_gemm.hip", "tile_schedule.h", "o2m_internal.h"):
         with open(os.path.join(ROOT, "paper_2609_05419_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -30,6 +30,7 @@
 // Bound: int8 MFMA.  Algorithmic work per launch = 2 m n k int8 ops per
 // product (counting the padded-free m, n, k of the problem).
 #include "o2m_internal.h"
+#include "tile_schedule.h"
 
 namespace o2m {
 namespace {
@@ -42,7 +43,6 @@ constexpr int kStageBuf = 2 * kStageBytes;       // A and B of one stage
 constexpr int kLoadsPerStage = 8;                // 16-byte direct loads per thread per stage
 constexpr int kPipeBytes = kStages * kStageBuf;
 constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
-constexpr int kGroupRows = 8;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -57,67 +57,22 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
     return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
 }
 
-// Tile schedule.  Each XCD has a queue of slots, and within a product the
-// slots follow a grouped order of the tiles (groups of 8 tile-rows,
-// column-major inside a group), cut into windows of 32 tiles (8 tile-rows x
-// 4 tile-columns): the tiles resident on one XCD at a time share their A and
-// B stages in that XCD's L2.  All XCDs sweep the batch items (one int8 GEMM
-// each) in the same order, so at any time the whole chip works on one
-// product.  Products whose planes fit in the 256 MB Infinity Cache give each
-// XCD one contiguous chunk of the order.  Larger ones (2 x 256 MB at 16384^2)
-// deal the windows round-robin (window w -> XCD w % 8), so that all XCDs work
-// in the same group of 8 tile-rows at once and its A strip is read once from
-// HBM and shared through the Infinity Cache.  Slots beyond a product's tiles
-// idle.
-struct TileCoord {
-    int p, ti, tj;
-    bool valid;
-};
-__device__ inline TileCoord tile_of(int x, int slot, int mt, int nt, int chunk, int deal) {
-    TileCoord c;
-    c.p = slot / chunk;
-    const int s = slot - c.p * chunk;  // the slot within the product
-    const int t = deal ? (8 * (s >> 5) + x) * 32 + (s & 31) : x * chunk + s;  // index in the grouped order
-    c.valid = t < mt * nt;
-    if (!c.valid) return c;  // idle slot (its group arithmetic would divide by zero)
-    const int group = t / (kGroupRows * nt);
-    const int first = group * kGroupRows;
-    const int gsize = min(mt - first, kGroupRows);
-    const int within = t - group * kGroupRows * nt;
-    c.ti = first + within % gsize;
-    c.tj = within / gsize;
-    return c;
-}
-
-// The XCDs of the part do not run at one clock (up to a tenth apart under
-// this load), so a fixed share of tiles per XCD would leave the fast ones idle
-// while the slowest finishes.  The first 7/8 of each XCD's slots therefore go
-// to workgroups by index, as dispatched (workgroup b runs on XCD b % 8 and
-// takes its slot b / 8), and the last 1/8 form a pool that workgroups claim
-// at run time: the next slot of the pool of their own XCD (the hardware
-// XCC_ID register names it), and once that is empty, the next slot of the
-// first other pool that still has one.  The launch carries spare workgroups
-// for those extra claims; a workgroup that finds every pool empty exits.
-// Only the pool's workgroups wait for an atomic round trip before their first
-// stage copy, and the spares cost a few microseconds at the end, so short
-// launches (fewer than 128 k-stages or 256 slots per XCD, where that cost
-// outweighs the balance) keep every slot fixed.  Each pool slot is handed out once (atomic counters, which
-// start at zero), and every one is claimed: a workgroup only finds all pools
-// empty when all their slots are taken, and the pools have more workgroups
-// than slots.
+// The tile schedule (tile_of, gemm_schedule) is in tile_schedule.h; the pool
+// of claimed slots is worked here.
 constexpr int kHwRegXccId = (31 << 11) | 20;  // s_getreg operand: all 32 bits of XCC_ID
 
 __device__ inline unsigned claim_next(unsigned *q) {
     return __hip_atomic_fetch_add(q, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Run by all lanes of one wave; returns x << 28 | slot, or -1 (wave-uniform).
+// Run by all lanes of one wave; returns x << kSlotBits | slot, or -1
+// (wave-uniform).
 // Pool x holds slots [S, slots) of XCD x; its counter counts the claims.
 __device__ inline int claim_slot(unsigned *queue, unsigned S, unsigned slots, int lane) {
     const int x = __builtin_amdgcn_s_getreg(kHwRegXccId) & 7;
     unsigned t = lane == 0 ? claim_next(queue + x * kQueueStride) : 0u;
     t = __builtin_amdgcn_readfirstlane(t);
-    if (t < slots - S) return (x << 28) | (int)(S + t);
+    if (t < slots - S) return (x << kSlotBits) | (int)(S + t);
     // own pool empty: look at the others all at once, then claim in turn
     const int y = (x + lane) & 7;
     const unsigned used =
@@ -130,7 +85,7 @@ __device__ inline int claim_slot(unsigned *queue, unsigned S, unsigned slots, in
         const int z = (x + i) & 7;
         t = lane == 0 ? claim_next(queue + z * kQueueStride) : 0u;
         t = __builtin_amdgcn_readfirstlane(t);
-        if (t < slots - S) return (z << 28) | (int)(S + t);
+        if (t < slots - S) return (z << kSlotBits) | (int)(S + t);
     }
     return -1;
 }
@@ -425,7 +380,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
         __syncthreads();
         const int c = *claimed;
         if (c < 0) return;  // whole workgroup: no barrier is pending
-        tc = tile_of(c >> 28, c & 0x0FFFFFFF, g.mt, g.nt, g.chunk, g.deal);
+        tc = tile_of(c >> kSlotBits, c & ((1 << kSlotBits) - 1), g.mt, g.nt, g.chunk, g.deal);
         if (!tc.valid) return;
         rA = rsrc_a(g, tc);
         rB = rsrc_b(g, tc);
@@ -465,23 +420,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
 hipError_t launch_gemm(const GemmArgs &ga_in, hipStream_t st) {
     static_assert(kThreads * 16 * kLoadsPerStage == 2 * kStageBytes, "stage copy covers A and B");
     GemmArgs ga = ga_in;
-    const long tiles = (long)ga.mt * ga.nt;
-    if (tiles <= 0 || ga.batch <= 0 || ga.kblocks <= 0) return hipSuccess;
-    // deal windows when each XCD gets at least two and one product's operand
-    // planes outgrow the 256 MB Infinity Cache
-    const long windows = (tiles + 31) / 32;
-    const long plane_bytes = (long)(ga.mt + ga.nt) * kStageBytes * ga.kblocks;
-    ga.deal = windows >= 16 && plane_bytes > (256L << 20) ? 1 : 0;
-    ga.chunk = ga.deal ? (int)(32 * ((windows + 7) / 8)) : (int)((tiles + 7) / 8);
-    const long total = 8L * ga.chunk * ga.batch;
-    if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
-    // pooled: the last 1/8 of each XCD's slots, plus one spare workgroup per
-    // 12 slots, so that a faster XCD can take slots of a slower one's pool
-    const long slots = ga.chunk * (long)ga.batch;
-    const bool pool = ga.kblocks >= 128 && slots >= 256;
-    ga.fixed = (int)(pool ? slots - slots / 8 : slots);
-    const long grid = total + (pool ? 8 * ((slots + 11) / 12) : 0);
-    if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const GemmSchedule sc = gemm_schedule(ga.mt, ga.nt, ga.kblocks, ga.batch, kStageBytes);
+    if (sc.grid == 0) return hipSuccess;
+    if (sc.grid > 0x7FFFFFFF || sc.slots >= (1L << kSlotBits)) return hipErrorInvalidValue;
+    ga.deal = sc.deal;
+    ga.chunk = sc.chunk;
+    ga.fixed = (int)sc.fixed;
+    const long grid = sc.grid;
     gemm_i8_kernel<<<(unsigned)grid, kThreads, 0, st>>>(ga);
     return hipGetLastError();
 }
