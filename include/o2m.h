@@ -67,6 +67,13 @@
  * Calls on one device share that workspace: calls that overlap in time on
  * different streams of the same device race.
  *
+ * Graph capture: once the workspace is large enough for a call (an earlier
+ * call of the same or a larger size, or o2m_set_workspace), the call enqueues
+ * kernels only (no allocation, no host synchronisation, no memset: buffers
+ * are cleared by kernels), so it can be captured into a HIP graph on its
+ * stream and replayed; each replay reads the captured input buffers anew.
+ * With phase timing on, the captured call records its events as well.
+ *
  * Return value: O2M_OK, or a negative code.  -1 .. -12: the position of the
  * first invalid argument (BLAS convention, counting from 1).  Errors found
  * before anything is enqueued leave C untouched.

@@ -504,6 +504,51 @@ def test_calls_on_a_side_stream(o2m):
     assert same_bits(np.asfortranarray(C2.cpu().numpy()), O.oq_zgemm(a, b, 12))
 
 
+def _graph_replays(o2m, m, n, k, N, seeds, entries=None):
+    """Capture one zgemm_2m call into a HIP graph and replay it on fresh
+    inputs copied into the captured buffers (eager copies and a sync between
+    replays); each replay must equal the oracle for the inputs it saw."""
+    A = o2m.colmajor(torch.zeros((m, k), dtype=torch.complex128, device=DEV))
+    B = o2m.colmajor(torch.zeros((k, n), dtype=torch.complex128, device=DEV))
+    o2m.zgemm_2m(A, B, n_moduli=N)  # sizes the workspace outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        C = o2m.zgemm_2m(A, B, n_moduli=N)
+    for seed in seeds:
+        a = W.complex_matrix(m, k, seed, dist="phi", phi=2.0)
+        b = W.complex_matrix(k, n, seed + 1, dist="phi", phi=2.0)
+        A.copy_(to_dev(a))
+        B.copy_(to_dev(b))
+        g.replay()
+        got = host(C)
+        if entries is None:
+            assert same_bits(got, O.oq_zgemm(a, b, N)), seed
+        else:
+            assert same_bits(np.array([got[i, j] for i, j in entries]), O.oq_zgemm(a, b, N, entries=entries)), seed
+
+
+def test_zgemm_in_a_hip_graph(o2m):
+    """The call is capturable: no host synchronisation, allocation or memset
+    once the workspace is sized; three replays on three inputs, bit-exact."""
+    print("[parity] graph replays 300x270x520 N=16", flush=True)
+    _graph_replays(o2m, 300, 270, 520, 16, seeds=(9401, 9403, 9405))
+
+
+@pytest.mark.slow
+def test_zgemm_pooled_in_a_hip_graph(o2m):
+    """As above at a shape whose int8 GEMM pools the last slots of each XCD:
+    the pool counters are cleared inside the graph (by the first kernel's
+    fill), so every replay claims from fresh pools; sampled entries in every
+    output tile, bit-exact."""
+    m, n, k = 8 * 256 - 21, 8 * 256 - 3, 8200
+    rng = np.random.default_rng(41)
+    ent = [(256 * ti + int(rng.integers(0, min(256, m - 256 * ti))),
+            256 * tj + int(rng.integers(0, min(256, n - 256 * tj)))) for ti in range(8) for tj in range(8)]
+    print(f"[parity] graph replays {m}x{n}x{k} N=16 (pooled)", flush=True)
+    _graph_replays(o2m, m, n, k, 16, seeds=(9411, 9413), entries=ent)
+
+
 def test_phase_timing(o2m):
     """The per-phase HIP events: four positive phase times averaged over the
     calls since enabling, a restart on re-enabling, nothing while disabled,
