@@ -256,12 +256,16 @@ __device__ inline void zero_acc(v4i (&acc)[8][8]) {
     acc_after_fill(acc);
 }
 
-// Fill the ring with the first min(KB, kStages) stages of one tile, wait for
-// stage 0 and read its fragments into (fa, fb).
-__device__ inline void prologue(const Wave &w, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB, int KB,
-                                v4i (&fa)[8], v4i (&fb)[8]) {
+// Fill the ring with the first min(KB, kStages) stages of one tile.
+__device__ inline void prologue_copies(const Wave &w, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rB,
+                                       int KB) {
     const int pre = KB < kStages ? KB : kStages;
     for (int s = 0; s < pre; ++s) load_stage(rA, rB, s, w.lds + s * kStageBuf, w.tid, w.wave);
+}
+
+// Wait for stage 0 of the ring and read its fragments into (fa, fb).
+__device__ inline void prologue_wait(const Wave &w, int KB, v4i (&fa)[8], v4i (&fb)[8]) {
+    const int pre = KB < kStages ? KB : kStages;
     switch (pre) {
     case 1: wait_vm<0>(); break;
     case 2: wait_vm<kLoadsPerStage>(); break;
@@ -360,36 +364,38 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_i8_kernel(GemmArgs g) {
 
     const Wave w = wave_of(lds);
     const int slots = g.chunk * g.batch;  // per XCD
+    // all arguments of the tile arithmetic and the first stage copies are
+    // loaded here in one round, rather than in rounds behind each other
+    asm volatile("" ::"s"(g.a), "s"(g.b), "s"(g.a_pstride), "s"(g.b_pstride), "s"(g.kblocks), "s"(g.mt),
+                 "s"(g.nt), "s"(g.deal), "s"(g.fixed));
     v4i acc[8][8];
     TileCoord tc;
     __amdgpu_buffer_rsrc_t rA, rB;
     if ((int)(blockIdx.x >> 3) < g.fixed) {
-        // the tile and its operands are worked out before the accumulator fill,
-        // so that the argument loads they need are not waited for behind it
         tc = tile_of(blockIdx.x & 7, blockIdx.x >> 3, g.mt, g.nt, g.chunk, g.deal);
         if (!tc.valid) return;  // whole workgroup: no barrier is pending
-        rA = rsrc_a(g, tc);
-        rB = rsrc_b(g, tc);
-        zero_acc(acc);
     } else {
         if (w.wave == 0) {
             const int r = claim_slot(g.queue, (unsigned)g.fixed, (unsigned)slots, w.lane);
             if (w.lane == 0) *claimed = r;
         }
-        zero_acc(acc);  // while the claim is in flight
         __syncthreads();
         const int c = *claimed;
         if (c < 0) return;  // whole workgroup: no barrier is pending
         tc = tile_of(c >> kSlotBits, c & ((1 << kSlotBits) - 1), g.mt, g.nt, g.chunk, g.deal);
         if (!tc.valid) return;
-        rA = rsrc_a(g, tc);
-        rB = rsrc_b(g, tc);
     }
+    rA = rsrc_a(g, tc);
+    rB = rsrc_b(g, tc);
     const int KB = g.kblocks;
-
+    // the first stage copies go out before the accumulator fill, which then
+    // runs while they are in flight
+    prologue_copies(w, rA, rB, KB);
+    sched_fence();
+    zero_acc(acc);
     // Fragments of the current stage (fa0, fb0) and of the next one.
     v4i fa0[8], fb0[8], fa1[8], fb1[8];
-    prologue(w, rA, rB, KB, fa0, fb0);
+    prologue_wait(w, KB, fa0, fb0);
 
     // Steady state, two stages per trip so that the fragment sets alternate
     // statically; then at most five stages with shrinking waits, the sets
