@@ -26,6 +26,11 @@
 // of its first 32 MFMAs and its 8 stage copies after every fourth of the last
 // 32: a memory instruction never waits behind another one in front of an
 // MFMA.  The residues leave straight from the accumulators.
+//
+// Which workgroup computes which tile is set out in tile_schedule.h: fixed
+// slots by workgroup index, and on long launches a pool of slots per XCD
+// that workgroups claim at run time (claim_slot below), so that XCDs running
+// at different clocks finish together.
 
 // Bound: int8 MFMA.  Algorithmic work per launch = 2 m n k int8 ops per
 // product (counting the padded-free m, n, k of the problem).

@@ -170,7 +170,7 @@ inline int residue_digits(int bits) {
 // dimension ldc = m_pad, plane stride ldc * n_pad.  mod[p], inv[p]: the
 // modulus of product p and its fp64 reciprocal.
 // The int8 GEMM's pool counters sit kQueueStride unsigned apart (256 bytes):
-// one cache line each, so that claims on different queues do not serialize.
+// one cache line each, so that claims on different pools do not serialize.
 constexpr int kQueueStride = 64;
 
 struct GemmArgs {
