@@ -38,8 +38,8 @@ template <> struct Digit<4> { typedef int type; };
 template <> struct Digit<5> { typedef int type; };
 
 // x = sum_d dg[d] 2^(26 d), peeled from the top digit down (each step exact).
-template <int D, typename DT>
-__device__ inline void split_digits(double x, DT (&dg)[D][16], int e) {
+template <int D, int PT, typename DT>
+__device__ inline void split_digits(double x, DT (&dg)[D][PT], int e) {
 #pragma unroll
     for (int d = D - 1; d >= 1; --d) {
         const double q = rint(ldexp(x, -26 * d));
@@ -84,7 +84,17 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
     return __builtin_amdgcn_perm(hi, lo, 0x05040100u);                // [lo.0, lo.1, hi.0, hi.1]
 }
 
-constexpr int kPerThread = 16;  // k entries per thread = one lane chunk of a fragment
+// k entries per thread: one lane chunk of a fragment (16), or half of one for
+// four and five digits, whose int32 digits would otherwise hold the kernel to
+// one wave per SIMD; the two halves of a fragment then go to two waves.
+template <int D> constexpr int per_thread() { return D >= 4 ? 8 : 16; }
+
+// PT residue bytes of one lane, contiguous in the plane (16- or 8-byte store).
+template <int PT>
+__device__ inline void store_words(int8_t *dst, const uint32_t (&w)[PT / 4]) {
+    if constexpr (PT == 16) *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+    else *reinterpret_cast<uint2 *>(dst) = make_uint2(w[0], w[1]);
+}
 
 // MODE 0: rows of X (A, column-major m x k): entry (r, kk) at X[r + kk*ld]
 // MODE 1: columns of X (B, column-major k x n): entry (r, kk) at X[kk + r*ld]
@@ -96,20 +106,23 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
                                                       int rows_pad, int kblocks, int plane_kblocks,
                                                       int kofs_p, int kofs_m, size_t plane_bytes,
                                                       ResidueParams rp, int8_t *planes) {
+    constexpr int PT = per_thread<D>();
+    constexpr int kHalves = 16 / PT;                          // waves per fragment
     const int lane = threadIdx.x & 63;
-    const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);   // one wave = one fragment
+    const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int frag = wave / kHalves, half = wave % kHalves;   // one fragment per kHalves waves
     const int frows = rows_pad / kFragRows;                   // fragments along rows
     const int fks = kblocks;                                  // fragments along k
     int fr, fk;
-    if (wave >= frows * fks) return;
-    if (MODE == 1) { fk = wave % fks; fr = wave / fks; }      // B: walk k fastest (contiguous)
-    else { fr = wave % frows; fk = wave / frows; }            // A: walk rows fastest
+    if (frag >= frows * fks) return;
+    if (MODE == 1) { fk = frag % fks; fr = frag / fks; }      // B: walk k fastest (contiguous)
+    else { fr = frag % frows; fk = frag / frows; }            // A: walk rows fastest
     const int r = fr * kFragRows + (lane & 15);
-    const int kk0 = fk * kStageK + (lane >> 4) * 16;
+    const int kk0 = fk * kStageK + (lane >> 4) * 16 + half * PT;
 
     // ---- load and quantize (step 3) -------------------------------------
     typedef typename Digit<D>::type DT;
-    DT xr[D][kPerThread], xi[D][kPerThread];
+    DT xr[D][PT], xi[D][PT];
     int sh = 0;
     bool live = r < rows;
     if (SCALED && live) {
@@ -118,7 +131,7 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
         else sh = shift - e;
     }
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) {
+    for (int e = 0; e < PT; ++e) {
         const int kk = kk0 + e;
         double vr = 0.0, vi = 0.0;
         if (live && kk < k) {
@@ -138,8 +151,8 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
             vr = rint(ldexp(vr, sh));
             vi = rint(ldexp(vi, sh));
         }
-        split_digits<D>(vr, xr, e);
-        split_digits<D>(vi, xi, e);
+        split_digits<D, PT>(vr, xr, e);
+        split_digits<D, PT>(vi, xi, e);
     }
 
     // ---- residues and 2M pre per modulus (step 4, eq. 2m-pre) -------------
@@ -149,9 +162,9 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
         const double inv = rp.inv[l];
         const double s = (double)rp.root[l];
         const uint32_t negm = (uint32_t)(-rp.mod[l]) & 0xFFFFFFu;
-        uint32_t wp[4], wm[4];
+        uint32_t wp[PT / 4], wm[PT / 4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < PT / 4; ++q) {
             uint32_t bp[4], bm[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
@@ -171,17 +184,17 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
             wp[q] = pack4(bp[0], bp[1], bp[2], bp[3]);
             wm[q] = pack4(bm[0], bm[1], bm[2], bm[3]);
         }
-        *reinterpret_cast<uint4 *>(dst_p + (size_t)(2 * l) * plane_bytes) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
-        *reinterpret_cast<uint4 *>(dst_m + (size_t)(2 * l) * plane_bytes) = make_uint4(wm[0], wm[1], wm[2], wm[3]);
+        store_words<PT>(dst_p + (size_t)(2 * l) * plane_bytes, wp);
+        store_words<PT>(dst_m + (size_t)(2 * l) * plane_bytes, wm);
     }
 
     // ---- hybrid sets: residues of Xr, Xi and Xr + Xi for 3M (Section 3.2) ---
     for (int l = rp.n2; l < rp.n; ++l) {
         const double inv = rp.inv[l];
         const uint32_t negm = (uint32_t)(-rp.mod[l]) & 0xFFFFFFu;
-        uint32_t w[3][4];
+        uint32_t w[3][PT / 4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < PT / 4; ++q) {
             uint32_t by[3][4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
@@ -205,7 +218,7 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
         const size_t p0 = (size_t)(2 * rp.n2 + 3 * (l - rp.n2));
 #pragma unroll
         for (int c = 0; c < 3; ++c)
-            *reinterpret_cast<uint4 *>(dst_p + (p0 + c) * plane_bytes) = make_uint4(w[c][0], w[c][1], w[c][2], w[c][3]);
+            store_words<PT>(dst_p + (p0 + c) * plane_bytes, w[c]);
     }
 }
 
@@ -215,7 +228,10 @@ hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const i
                            int digits, int khalf, const PlaneGeom &g, const ResidueParams &rp,
                            int8_t *planes, hipStream_t st) {
     const int kreal = khalf > 0 ? g.kreal : 0;
-    const long waves = (long)(g.rows_pad / kFragRows) * (long)g.kblocks;
+    // waves: one per fragment, two for four and five digits (per_thread)
+    const long frags = (long)(g.rows_pad / kFragRows) * (long)g.kblocks;
+    const long waves = frags * (digits >= 4 ? 2 : 1);
+    if ((waves + 3) / 4 > 0x7FFFFFFF) return hipErrorInvalidValue;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
 #define O2M_RES(M, T, DD, SC)                                                                    \
     residue_kernel<M, T, DD, SC><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k,     \

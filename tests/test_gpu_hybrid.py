@@ -44,6 +44,11 @@ CASES = [
     (33, 47, 65, "normal", 0.5, 32, "max"),
     (70, 90, 300, "phi", 2.0, 25, "cs"),
     (5, 3, 1, "normal", 0.5, 32, "cs"),
+    # quantized values beyond 2^88: four base-2^26 digits (pA, pB 98..106),
+    # then five (pA 110); their residues are computed by two waves per fragment
+    (257, 130, 300, "phi", 2.0, 29, "max"),
+    (130, 301, 1000, "normal", 0.5, 31, "max"),
+    (200, 150, 130, "phi", 2.0, 32, "max"),
 ]
 
 
