@@ -421,6 +421,28 @@ def test_zgemm_pooled_tiles_sampled(o2m):
 
 
 @pytest.mark.slow
+def test_zgemm_pooled_with_idle_slots_sampled(o2m):
+    """19 x 3 = 57 tiles per product (not a multiple of the 8 XCDs, so every
+    product leaves 7 idle slots, some of them in the pools) with 129 k-stages
+    and 32 products: pooled launch.  Two sampled entries in each of the 57
+    output tiles, bit-exact."""
+    m, n, k = 19 * 256 - 5, 3 * 256 - 9, 8200
+    a = W.complex_matrix(m, k, 9501)
+    b = W.complex_matrix(k, n, 9502)
+    print(f"[parity] pooled with idle slots {m}x{n}x{k} N=16", flush=True)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    rng = np.random.default_rng(51)
+    ent = [(m - 1, n - 1)]
+    for ti in range(19):
+        for tj in range(3):
+            for _ in range(2):
+                ent.append((256 * ti + int(rng.integers(0, min(256, m - 256 * ti))),
+                            256 * tj + int(rng.integers(0, min(256, n - 256 * tj)))))
+    got = np.array([C[i, j] for i, j in ent])
+    assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
+
+
+@pytest.mark.slow
 def test_zgemm_tall_skinny_sampled(o2m):
     """m = n = 4096, k = 65536 (N = 16): int32 headroom and the long k-loop."""
     m, n, k = 4096, 4096, 65536
