@@ -1,6 +1,8 @@
 """GPU parity of hybrid 2M/3M moduli sets (Section 3.2: beyond the 22 2M moduli,
 3M per modulus) with the CPU oracle, through the C-ABI: bit-exact results,
 exact per-modulus residues, and the accuracy the extra moduli buy."""
+import os
+
 import numpy as np
 import pytest
 
@@ -163,11 +165,12 @@ def test_zgemm_8192_hybrid_sampled(o2m):
 def test_randomized_configurations(o2m):
     """Seeded random combinations of call, shape, moduli count, scaling rule and
     input distribution, each bit-exact against the oracle (a sweep over the
-    corners the fixed cases do not combine)."""
-    rng = np.random.default_rng(2609)
+    corners the fixed cases do not combine).  O2M_RANDOM_CASES and
+    O2M_RANDOM_SEED widen the sweep (default: 36 cases, seed 2609)."""
+    rng = np.random.default_rng(int(os.environ.get("O2M_RANDOM_SEED", "2609")))
     ops = ["zgemm", "cgemm", "zherk", "dsyrk", "zher2k", "dsyr2k"]
     low = lambda n: np.tril(np.ones((n, n), dtype=bool))
-    for case in range(36):
+    for case in range(int(os.environ.get("O2M_RANDOM_CASES", "36"))):
         op = ops[case % len(ops)]
         sym = op not in ("zgemm", "cgemm")
         N = int(rng.integers(1, 23 if sym else 33))
