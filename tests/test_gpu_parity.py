@@ -7,6 +7,7 @@ Accuracy against the unquantized product (double-double reference) is checked
 separately with the tolerance 4 u k |A||B| (u = 2^-53 for ZGEMM, 2^-24 for
 CGEMM)."""
 import math
+import os
 
 import numpy as np
 import pytest
@@ -440,6 +441,34 @@ def test_zgemm_pooled_with_idle_slots_sampled(o2m):
                             256 * tj + int(rng.integers(0, min(256, n - 256 * tj)))))
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
+
+
+@pytest.mark.slow
+def test_zgemm_pooled_random_shapes(o2m):
+    """Random ragged shapes with k >= 8129 (the int8 GEMM's claimed pool in
+    use), moduli counts 8..22 and both scaling rules; two sampled entries in
+    every output tile and the corners, bit-exact.  O2M_POOLED_CASES and
+    O2M_POOLED_SEED widen the sweep (default: 4 cases, seed 777)."""
+    rng = np.random.default_rng(int(os.environ.get("O2M_POOLED_SEED", "777")))
+    for case in range(int(os.environ.get("O2M_POOLED_CASES", "4"))):
+        m, n = (int(x) for x in rng.integers(256, 2600, 2))
+        k = int(rng.choice([8200, 9001, 10240, 12000]))
+        N = int(rng.integers(8, 23))
+        rule = "cs" if rng.random() < 0.3 else "max"
+        if rule == "cs" and O.budget_cs(O.moduli_set(N), k, False) is None:
+            rule = "max"
+        a = W.complex_matrix(m, k, 20000 + case, dist="phi", phi=float(rng.choice([0.5, 2.0])))
+        b = W.complex_matrix(k, n, 30000 + case)
+        print(f"[parity] pooled random case {case}: {m}x{n}x{k} N={N} {rule}", flush=True)
+        C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+        ent = [(m - 1, n - 1), (0, 0)]
+        for ti in range(-(-m // 256)):
+            for tj in range(-(-n // 256)):
+                for _ in range(2):
+                    ent.append((256 * ti + int(rng.integers(0, min(256, m - 256 * ti))),
+                                256 * tj + int(rng.integers(0, min(256, n - 256 * tj)))))
+        got = np.array([C[i, j] for i, j in ent])
+        assert same_bits(got, O.oq_zgemm(a, b, N, entries=ent, scaling=rule)), case
 
 
 @pytest.mark.slow
