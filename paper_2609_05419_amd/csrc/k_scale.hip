@@ -91,7 +91,7 @@ __device__ inline unsigned long long ssq_term(double v, int e) {
     return q * q;
 }
 
-constexpr int kRowChunk = 64;     // columns per thread in row mode (at most)
+constexpr int kRowChunk = 128;    // columns per thread in row mode (at most)
 constexpr int kColChunk = 2048;   // rows per block in column mode
 
 template <ElemType ET>
@@ -215,7 +215,10 @@ __global__ void zero_matrix_kernel(unsigned char *c, int rows_bytes, int n, size
 }  // namespace
 
 // Columns per thread in row mode: kRowChunk, fewer (down to 8) when the
-// grid would otherwise hold fewer than ~2048 blocks (small matrices).
+// grid would otherwise hold fewer than ~2048 blocks (small matrices).  Each
+// block ends in one atomicMax per row, so longer chunks mean fewer atomics on
+// the same addresses (128 rather than 64 columns: the scaling phase of a
+// 8192^3 complex call 0.405 -> 0.392 ms).
 int row_chunk(int rows, int cols) {
     const long rb = (rows + 255) / 256;
     int chunk = kRowChunk;
