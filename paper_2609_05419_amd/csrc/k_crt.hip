@@ -24,6 +24,7 @@
 // written (complex fp64; 8 for complex fp32).
 #include "o2m_internal.h"
 #include "crt_round.h"
+#include "sym_schedule.h"
 
 #include <type_traits>
 
@@ -191,13 +192,20 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
 // tile of the lower triangle and stages both tiles of every plane in LDS.
 template <int T, bool REAL_ONLY>
 __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
-    __shared__ __attribute__((aligned(16))) int8_t tp[2][32 * 32];
-    __shared__ __attribute__((aligned(16))) int8_t tq[2][32 * 32];
-    const int nb = (a.n + 31) / 32;
-    const int I = blockIdx.x % nb, J = blockIdx.x / nb;
-    if (I < J) return;  // strictly upper tiles: nothing to write
+    // [buffer][P = C+ tile (I, J), Q = C+ tile (J, I)], column-major 32 x 32
+    __shared__ __attribute__((aligned(16))) int8_t tl[2][2][32 * 32];
+    const SymTile st = sym_tile_of(blockIdx.x, (a.n + 31) / 32);
+    if (!st.valid) return;  // idle slot or strictly upper tile: nothing to write
+    const int I = st.I, J = st.J;
     const int tid = threadIdx.x;
     const int jl = tid >> 3, il0 = (tid & 7) * 4;
+
+    // threads 0..127 copy 16 bytes of each plane: half a column of P or of Q
+    const bool loader = tid < 128;
+    const int q = tid >> 6, c = (tid & 63) >> 1, h = tid & 1;
+    const int8_t *src = a.res + (q == 0 ? (size_t)(J * 32 + c) * a.ldr + I * 32 + h * 16
+                                        : (size_t)(I * 32 + c) * a.ldr + J * 32 + h * 16);
+    const int dst = c * 32 + h * 16;
 
     double sre[4][T], sim[4][T];
 #pragma unroll
@@ -205,24 +213,23 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
+    // the next plane's copy is in flight while this plane's limb sums run; two
+    // LDS buffers, so one barrier per plane orders both the writes before the
+    // reads and the reads of plane l - 2 before the writes of plane l
+    uint4 next = make_uint4(0, 0, 0, 0);
+    if (loader) next = *reinterpret_cast<const uint4 *>(src);
     for (int l = 0; l < cp.n; ++l) {
         const int buf = l & 1;
-        const int8_t *plane = a.res + (size_t)l * a.plane_bytes;
-        if (tid < 64) {          // P = C+[I rows, J cols]
-            const int c = tid >> 1, h = tid & 1;
-            *reinterpret_cast<uint4 *>(&tp[buf][c * 32 + h * 16]) =
-                *reinterpret_cast<const uint4 *>(plane + (size_t)(J * 32 + c) * a.ldr + I * 32 + h * 16);
-        } else if (tid < 128) {  // Q = C+[J rows, I cols]
-            const int c = (tid - 64) >> 1, h = tid & 1;
-            *reinterpret_cast<uint4 *>(&tq[buf][c * 32 + h * 16]) =
-                *reinterpret_cast<const uint4 *>(plane + (size_t)(I * 32 + c) * a.ldr + J * 32 + h * 16);
+        if (loader) {
+            *reinterpret_cast<uint4 *>(&tl[buf][q][dst]) = next;
+            if (l + 1 < cp.n) next = *reinterpret_cast<const uint4 *>(src + (size_t)(l + 1) * a.plane_bytes);
         }
         __syncthreads();
-        const uint32_t wp = *reinterpret_cast<const uint32_t *>(&tp[buf][jl * 32 + il0]);
+        const uint32_t wp = *reinterpret_cast<const uint32_t *>(&tl[buf][0][jl * 32 + il0]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int rp = sext8(wp, e);                       // C+[i, j]
-            const int rm = (int)tq[buf][(il0 + e) * 32 + jl];  // C-[i, j] = C+[j, i]
+            const int rp = sext8(wp, e);                          // C+[i, j]
+            const int rm = (int)tl[buf][1][(il0 + e) * 32 + jl];  // C-[i, j] = C+[j, i]
             const double u = (double)(rm + rp), v = (double)(rm - rp);
 #pragma unroll
             for (int t = 0; t < T; ++t) {
@@ -255,10 +262,10 @@ template <int T>
 hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &cp, hipStream_t st) {
     if (mode == 1 || mode == 2) {
         if (T > 4 || cp.n2 != cp.n) return hipErrorInvalidValue;  // symmetric ops: 2M moduli only
-        const int nb = (ca.n + 31) / 32;
-        const unsigned blocks = (unsigned)nb * (unsigned)nb;
-        if (mode == 1) crt_sym_kernel<T, false><<<blocks, 256, 0, st>>>(ca, cp);
-        else crt_sym_kernel<T, true><<<blocks, 256, 0, st>>>(ca, cp);
+        const long blocks = sym_grid((ca.n + 31) / 32);
+        if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+        if (mode == 1) crt_sym_kernel<T, false><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+        else crt_sym_kernel<T, true><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
         return hipGetLastError();
     }
     // 4 rows of one column per thread, 1024 rows per workgroup

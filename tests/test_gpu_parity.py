@@ -246,7 +246,8 @@ def test_cgemm_tolerance(o2m):
 # ------------------------------------------------------------------ HERK / SYRK
 
 
-@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((257, 64), 8), ((33, 500), 20), ((1, 3), 16)])
+@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((257, 64), 8), ((33, 500), 20), ((1, 3), 16), ((161, 90), 13),
+                                     ((96, 40), 3)])
 def test_zherk_bit_exact_lower_triangle(o2m, shape, N):
     n, k = shape
     a = W.complex_matrix(n, k, 81 + n, dist="phi", phi=1.0)
@@ -261,7 +262,7 @@ def test_zherk_bit_exact_lower_triangle(o2m, shape, N):
     assert (np.diag(got).imag == 0).all()
 
 
-@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((70, 65), 16), ((257, 1), 8), ((40, 300), 22)])
+@pytest.mark.parametrize("shape,N", [((100, 130), 16), ((70, 65), 16), ((257, 1), 8), ((40, 300), 22), ((130, 77), 9)])
 def test_dsyrk_bit_exact_lower_triangle(o2m, shape, N):
     n, k = shape
     a = W.real_matrix(n, k, 91 + k)

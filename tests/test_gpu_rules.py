@@ -169,7 +169,7 @@ def test_cs_accuracy_curve_phi2(o2m):
 
 
 H2_CASES = [((100, 130), 16, "max"), ((257, 64), 8, "max"), ((33, 500), 22, "max"), ((1, 3), 16, "max"),
-            ((300, 70), 16, "cs"), ((65, 129), 20, "cs")]
+            ((300, 70), 16, "cs"), ((65, 129), 20, "cs"), ((129, 66), 15, "max"), ((70, 33), 21, "cs")]
 
 
 @pytest.mark.parametrize("shape,N,rule", H2_CASES, ids=[f"{c[0][0]}x{c[0][1]}-N{c[1]}-{c[2]}" for c in H2_CASES])

@@ -2,8 +2,12 @@
 maps to a distinct tile or idles, every tile of every product has a slot, the
 launch parameters keep their invariants, and a model of the run-time claims
 (fixed slots by workgroup index, per-XCD pools with stealing, spare
-workgroups; random XCD speeds) computes every tile exactly once."""
+workgroups; random XCD speeds) computes every tile exactly once.  And of the
+symmetric CRT's (sym_schedule.h): every lower-triangle tile has exactly one
+workgroup, and the four tiles that share a column line of either operand tile
+run on one XCD."""
 import ctypes
+import math
 import os
 import subprocess
 
@@ -24,6 +28,10 @@ def lib(tmp_path_factory):
     L.t_schedule.argtypes = [I, I, I, I, Lg, P]
     L.t_tile_of.argtypes = [I, I, I, I, I, I, P]
     L.t_all_tiles.argtypes = [I, I, I, I, Lg, P]
+    L.t_sym_grid.argtypes = [I]
+    L.t_sym_grid.restype = Lg
+    L.t_sym_tiles.argtypes = [I, Lg, P]
+    L.t_sym_tile_of.argtypes = [Lg, I, P]
     return L
 
 
@@ -144,3 +152,44 @@ def test_claimed_run_computes_every_tile_once(lib, shape):
         assert (done == 1).all(), (trial, int((done == 0).sum()), int((done > 1).sum()))
         # every slot went to exactly one workgroup, so exactly the spares came away empty
         assert empty == s["grid"] - 8 * s["slots"]
+
+
+SYM_NB = [0, 1, 2, 3, 4, 5, 7, 8, 9, 31, 32, 33, 63, 64, 65, 127, 255, 256, 257, 1000]
+
+
+@pytest.mark.parametrize("nb", SYM_NB)
+def test_sym_tiles_cover_lower_triangle_once(lib, nb):
+    grid = lib.t_sym_grid(nb)
+    ns = -(-nb // 4)
+    assert grid == 8 * 16 * -(-(ns * (ns + 1) // 2) // 8)
+    t = np.zeros((max(grid, 1), 3), dtype=np.int32)
+    lib.t_sym_tiles(nb, grid, t.ctypes.data)
+    t = t[:grid]
+    v = t[:, 0].astype(bool)
+    I, J = t[v, 1], t[v, 2]
+    assert len(I) == nb * (nb + 1) // 2
+    assert (I < nb).all() and (J >= 0).all() and (I >= J).all()
+    assert len(set(zip(I.tolist(), J.tolist()))) == len(I)
+    # the tiles sharing a line: same J, I // 4 (own tile) and same I, J // 4
+    # (mirrored tile) -- all in one super-tile on one XCD, in 16 consecutive slots
+    b = np.nonzero(v)[0]
+    key = (I // 4) * (ns + 1) + J // 4
+    for k in np.unique(key):
+        members = b[key == k]
+        assert len(set((members % 8).tolist())) == 1
+        slots = members // 8
+        assert slots.max() - slots.min() < 16 and len(set((slots // 16).tolist())) == 1
+
+
+def test_sym_tile_of_large_grids(lib):
+    # super-tile rows near triangular numbers, where a float square root could round
+    # the row index the wrong way
+    nb = 1 << 22
+    out = np.zeros(3, dtype=np.int32)
+    for k in (1, 2, 3, 1000, 46340, 46341, 1 << 19, (1 << 20) - 1):
+        for s in (k * (k + 1) // 2 - 1, k * (k + 1) // 2, k * (k + 1) // 2 + 1):
+            b = (s // 8) * 128 + s % 8  # the first workgroup (sub-tile 0) of super-tile s
+            lib.t_sym_tile_of(b, nb, out.ctypes.data)
+            si = (math.isqrt(8 * s + 1) - 1) // 2  # exact integer square root
+            assert (out[1], out[2]) == (4 * si, 4 * (s - si * (si + 1) // 2)), (k, s)
+            assert out[0] == 1

@@ -1,6 +1,8 @@
-// Host build of the int8 GEMM's tile schedule, for tests/test_tile_schedule.py.
+// Host build of the int8 GEMM's and the symmetric CRT's tile schedules, for
+// tests/test_tile_schedule.py.
 #define O2M_HD
 #include "../paper_2609_05419_amd/csrc/tile_schedule.h"
+#include "../paper_2609_05419_amd/csrc/sym_schedule.h"
 
 extern "C" {
 // deal, chunk, slots, fixed, grid
@@ -34,4 +36,21 @@ void t_all_tiles(int mt, int nt, int chunk, int deal, long slots, int *tiles) {
 }
 int t_xcds() { return o2m::kXcds; }
 int t_slot_bits() { return o2m::kSlotBits; }
+// Symmetric CRT: the launch's workgroup count, and tiles[3 * b + {valid, I, J}]
+// for each of its workgroups.
+long t_sym_grid(int nb) { return o2m::sym_grid(nb); }
+void t_sym_tiles(int nb, long grid, int *tiles) {
+    for (long b = 0; b < grid; ++b) {
+        const o2m::SymTile t = o2m::sym_tile_of(b, nb);
+        tiles[3 * b] = t.valid;
+        tiles[3 * b + 1] = t.I;
+        tiles[3 * b + 2] = t.J;
+    }
+}
+void t_sym_tile_of(long b, int nb, int *out) {
+    const o2m::SymTile t = o2m::sym_tile_of(b, nb);
+    out[0] = t.valid;
+    out[1] = t.I;
+    out[2] = t.J;
+}
 }
