@@ -55,8 +55,16 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     const int mblocks = (a.m + rows_per_block - 1) / rows_per_block;
     const int j = blockIdx.x / mblocks;
     const int i0 = ((blockIdx.x % mblocks) * 256 + threadIdx.x) * R;
-    if (i0 >= a.m) return;
-    const int8_t *base = a.res + (size_t)j * a.ldr + i0;
+    // complex fp64 outputs pass through LDS (each wave its own 256 entries) and
+    // leave in row order, so a lane may store rows of another lane: a wave
+    // leaves only when all its rows are beyond m, and a lane beyond m reads
+    // row 0 instead (its sums are never stored).  For complex fp32 outputs the
+    // detour cost more than the wider stores gained.
+    constexpr bool STAGE = MODE == 0 && OT == kF64;
+    __shared__ double2 stage[STAGE ? 256 * R : 1];
+    const int lane = threadIdx.x & 63, w0 = threadIdx.x & ~63;
+    if ((STAGE ? i0 - lane * R : i0) >= a.m) return;
+    const int8_t *base = a.res + (size_t)j * a.ldr + (i0 < a.m ? i0 : 0);
 
     if (MODE == 4) {
         for (int l = 0; l < cp.n; ++l) {
@@ -154,7 +162,7 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     for (int e = 0; e < R; ++e) {
         const int i = i0 + e;
         if (i >= a.m) break;
-        if (MODE == 3) {
+        if constexpr (MODE == 3) {
             const auto vre = lift_exact<T>(sre[e], cp.mlimb, cp.inv_m);
             const auto vim = lift_exact<T>(sim[e], cp.mlimb, cp.inv_m);
             // exact Gaussian integers: M < 2^63, fix the lift into [-h, h]
@@ -182,7 +190,20 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
                 re = lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
                 im = lift_round<T>(sim[e], cp.mlimb, cp.inv_m, sc);
             }
-            Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, re, im);
+            if constexpr (STAGE) stage[threadIdx.x * R + e] = make_double2(re, im);
+            else Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, re, im);
+        }
+    }
+    if constexpr (STAGE) {
+        // the wave's 256 rows leave in row order, 64 consecutive rows per store
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        const int ib = (blockIdx.x % mblocks) * rows_per_block + w0 * R;
+#pragma unroll
+        for (int e = 0; e < R; ++e) {
+            const int i = ib + e * 64 + lane;
+            const double2 v = stage[w0 * R + e * 64 + lane];
+            if (i < a.m) Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, v.x, v.y);
         }
     }
 }
@@ -198,7 +219,9 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     if (!st.valid) return;  // idle slot or strictly upper tile: nothing to write
     const int I = st.I, J = st.J;
     const int tid = threadIdx.x;
-    const int jl = tid >> 3, il0 = (tid & 7) * 4;
+    // the thread's entries: rows r0 + 8e (e = 0..3) of column jl, so that each
+    // store writes whole 128-byte lines across 8 lanes
+    const int jl = tid >> 3, r0 = tid & 7;
 
     // threads 0..127 copy 16 bytes of each plane: half a column of P or of Q
     const bool loader = tid < 128;
@@ -225,11 +248,10 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
             if (l + 1 < cp.n) next = *reinterpret_cast<const uint4 *>(src + (size_t)(l + 1) * a.plane_bytes);
         }
         __syncthreads();
-        const uint32_t wp = *reinterpret_cast<const uint32_t *>(&tl[buf][0][jl * 32 + il0]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int rp = sext8(wp, e);                          // C+[i, j]
-            const int rm = (int)tl[buf][1][(il0 + e) * 32 + jl];  // C-[i, j] = C+[j, i]
+            const int rp = (int)tl[buf][0][jl * 32 + r0 + 8 * e];    // C+[i, j]
+            const int rm = (int)tl[buf][1][(r0 + 8 * e) * 32 + jl];  // C-[i, j] = C+[j, i]
             const double u = (double)(rm + rp), v = (double)(rm - rp);
 #pragma unroll
             for (int t = 0; t < T; ++t) {
@@ -242,7 +264,7 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     const int j = J * 32 + jl;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const int i = I * 32 + il0 + e;
+        const int i = I * 32 + r0 + 8 * e;
         if (i >= a.n || j >= a.n || i < j) continue;
         const int ei = a.E[i], ej = a.E[j];
         const bool bad = ei == INT32_MIN || ej == INT32_MIN;
