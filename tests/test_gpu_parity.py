@@ -528,6 +528,53 @@ def test_zgemm_strided_operands_and_output(o2m):
     assert (got[m:, :] == 9.0 + 9j).all()           # rows beyond m untouched
 
 
+
+# the CRT stores whole lines: complex fp64 results leave each wave in row
+# order (a lane stores rows computed by other lanes), HERK/SYRK threads own
+# rows r, r + 8, r + 16, r + 24 of a tile column.  Row counts around the wave
+# (256 rows) and tile (32, 128) boundaries, with a padded ldc whose extra rows
+# (and, for HERK/SYRK, the upper triangle) must stay untouched.
+@pytest.mark.parametrize("m", [1, 63, 64, 65, 255, 256, 257, 1023, 1025, 1100])
+def test_zgemm_ragged_rows_padded_ldc(o2m, m):
+    n, k, pad = 3, 40, 37
+    a = W.complex_matrix(m, k, 430 + m)
+    b = W.complex_matrix(k, n, 431)
+    Cbig = o2m.colmajor(torch.full((m + pad, n), -5.0 + 2j, dtype=torch.complex128, device=DEV))
+    o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16, out=Cbig[:m, :])
+    got = host(Cbig)
+    assert same_bits(np.asfortranarray(got[:m, :]), O.oq_zgemm(a, b, 16))
+    assert (got[m:, :] == -5.0 + 2j).all()
+
+
+@pytest.mark.parametrize("m", [65, 257, 1025])
+def test_cgemm_ragged_rows_padded_ldc(o2m, m):
+    n, k, pad = 2, 33, 11
+    a = W.complex_matrix(m, k, 440 + m, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(k, n, 441, dist="uniform", dtype=np.complex64)
+    Cbig = o2m.colmajor(torch.full((m + pad, n), 3.0 - 1j, dtype=torch.complex64, device=DEV))
+    o2m.cgemm_2m(to_dev(a), to_dev(b), n_moduli=8, out=Cbig[:m, :])
+    got = host(Cbig)
+    assert same_bits(np.asfortranarray(got[:m, :]), O.oq_cgemm(a, b, 8))
+    assert (got[m:, :] == 3.0 - 1j).all()
+
+
+@pytest.mark.parametrize("n,N", [(1, 16), (31, 16), (33, 7), (127, 16), (129, 13), (200, 16)])
+def test_zherk_dsyrk_ragged_padded_ldc(o2m, n, N):
+    k, pad = 20, 9
+    a = W.complex_matrix(n, k, 450 + n)
+    Cbig = o2m.colmajor(torch.full((n + pad, n), 6.5 - 0.5j, dtype=torch.complex128, device=DEV))
+    o2m.zherk_2m(to_dev(a), n_moduli=N, out=Cbig[:n, :])
+    got = host(Cbig)
+    low = np.tril(np.ones((n, n), dtype=bool))
+    assert same_bits(got[:n, :][low], O.oq_zherk(a, N)[low])
+    assert (got[:n, :][~low] == 6.5 - 0.5j).all() and (got[n:, :] == 6.5 - 0.5j).all()
+    r = W.real_matrix(n, 2 * k + 1, 460 + n)
+    Rbig = o2m.colmajor(torch.full((n + pad, n), -4.25, dtype=torch.float64, device=DEV))
+    o2m.dsyrk_2m(to_dev(r), n_moduli=N, out=Rbig[:n, :])
+    gotr = host(Rbig)
+    assert same_bits(gotr[:n, :][low], O.oq_dsyrk(r, N)[low])
+    assert (gotr[:n, :][~low] == -4.25).all() and (gotr[n:, :] == -4.25).all()
+
 def test_cgemm_and_zherk_strided(o2m):
     a = W.complex_matrix(40, 33, 411, dist="uniform", dtype=np.complex64)
     b = W.complex_matrix(33, 21, 412, dist="uniform", dtype=np.complex64)
