@@ -166,8 +166,12 @@ def test_randomized_configurations(o2m):
     """Seeded random combinations of call, shape, moduli count, scaling rule and
     input distribution, each bit-exact against the oracle (a sweep over the
     corners the fixed cases do not combine).  O2M_RANDOM_CASES and
-    O2M_RANDOM_SEED widen the sweep (default: 36 cases, seed 2609)."""
+    O2M_RANDOM_SEED widen the sweep (default: 36 cases, seed 2609);
+    O2M_RANDOM_TALL=1 draws m up to 1300 (several 256-row waves of the CRT's
+    row-order stores, several 128 x 128 super-tiles of the symmetric CRT) with
+    n and k up to 200 instead of all three up to 300."""
     rng = np.random.default_rng(int(os.environ.get("O2M_RANDOM_SEED", "2609")))
+    tall = os.environ.get("O2M_RANDOM_TALL") == "1"
     ops = ["zgemm", "cgemm", "zherk", "dsyrk", "zher2k", "dsyr2k"]
     low = lambda n: np.tril(np.ones((n, n), dtype=bool))
     for case in range(int(os.environ.get("O2M_RANDOM_CASES", "36"))):
@@ -175,7 +179,11 @@ def test_randomized_configurations(o2m):
         sym = op not in ("zgemm", "cgemm")
         N = int(rng.integers(1, 23 if sym else 33))
         rule = "cs" if rng.random() < 0.5 else "max"
-        m, n, k = (int(x) for x in rng.integers(1, 300, 3))
+        if tall:
+            m = int(rng.integers(1, 1300))
+            n, k = (int(x) for x in rng.integers(1, 200, 2))
+        else:
+            m, n, k = (int(x) for x in rng.integers(1, 300, 3))
         k = max(1, k)
         if rule == "cs" and O.budget_cs(O.moduli_set(N), 2 * k if op in ("zher2k", "dsyr2k") else k, sym) is None:
             rule = "max"
