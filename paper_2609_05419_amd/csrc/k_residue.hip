@@ -86,7 +86,7 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
 
 // k entries per thread: one lane chunk of a fragment (16), or half of one for
 // four and five digits, whose int32 digits would otherwise hold the kernel to
-// one wave per SIMD; the two halves of a fragment then go to two waves.
+// one wave per SIMD; a fragment then goes to two waves, 32 chunks each.
 template <int D> constexpr int per_thread() { return D >= 4 ? 8 : 16; }
 
 // PT residue bytes of one lane, contiguous in the plane (16- or 8-byte store).
@@ -117,8 +117,13 @@ __global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, con
     if (frag >= frows * fks) return;
     if (MODE == 1) { fk = frag % fks; fr = frag / fks; }      // B: walk k fastest (contiguous)
     else { fr = frag % frows; fk = frag / frows; }            // A: walk rows fastest
-    const int r = fr * kFragRows + (lane & 15);
-    const int kk0 = fk * kStageK + (lane >> 4) * 16 + half * PT;
+    // the fragment's 16-byte lane chunk and the part of it this lane fills;
+    // with two waves per fragment each takes 32 whole chunks (adjacent lanes
+    // fill the two halves of one), so that a store covers 512 contiguous bytes
+    const int chunk = kHalves == 1 ? lane : half * 32 + (lane >> 1);
+    const int part = kHalves == 1 ? 0 : lane & 1;
+    const int r = fr * kFragRows + (chunk & 15);
+    const int kk0 = fk * kStageK + (chunk >> 4) * 16 + part * PT;
 
     // ---- load and quantize (step 3) -------------------------------------
     typedef typename Digit<D>::type DT;
