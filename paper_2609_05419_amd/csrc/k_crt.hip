@@ -45,6 +45,17 @@ template <> struct Out<kF32> {
     }
 };
 
+// An output entry as staged in LDS: the stored type itself.
+template <ElemType OT> struct Staged;
+template <> struct Staged<kF64> {
+    typedef double2 type;
+    static __device__ inline type make(double re, double im) { return make_double2(re, im); }
+};
+template <> struct Staged<kF32> {
+    typedef float2 type;
+    static __device__ inline type make(double re, double im) { return make_float2((float)re, (float)im); }
+};
+
 // MODE 0: ZGEMM / CGEMM output.  MODE 3: exact Gaussian integers (int64).
 // MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R = 4
 // consecutive rows of one column: one dword per plane.
@@ -55,13 +66,13 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     const int mblocks = (a.m + rows_per_block - 1) / rows_per_block;
     const int j = blockIdx.x / mblocks;
     const int i0 = ((blockIdx.x % mblocks) * 256 + threadIdx.x) * R;
-    // complex fp64 outputs pass through LDS (each wave its own 256 entries) and
-    // leave in row order, so a lane may store rows of another lane: a wave
-    // leaves only when all its rows are beyond m, and a lane beyond m reads
-    // row 0 instead (its sums are never stored).  For complex fp32 outputs the
-    // detour cost more than the wider stores gained.
-    constexpr bool STAGE = MODE == 0 && OT == kF64;
-    __shared__ double2 stage[STAGE ? 256 * R : 1];
+    // complex outputs pass through LDS in their stored type (each wave its own
+    // 256 entries) and leave in row order, so a lane may store rows of another
+    // lane: a wave leaves only when all its rows are beyond m, and a lane
+    // beyond m reads row 0 instead (its sums are never stored)
+    constexpr bool STAGE = MODE == 0;
+    typedef typename Staged<OT == kF32 ? kF32 : kF64>::type SV;
+    __shared__ SV stage[STAGE ? 256 * R : 1];
     const int lane = threadIdx.x & 63, w0 = threadIdx.x & ~63;
     if ((STAGE ? i0 - lane * R : i0) >= a.m) return;
     const int8_t *base = a.res + (size_t)j * a.ldr + (i0 < a.m ? i0 : 0);
@@ -190,7 +201,7 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
                 re = lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
                 im = lift_round<T>(sim[e], cp.mlimb, cp.inv_m, sc);
             }
-            if constexpr (STAGE) stage[threadIdx.x * R + e] = make_double2(re, im);
+            if constexpr (STAGE) stage[threadIdx.x * R + e] = Staged<OT == kF32 ? kF32 : kF64>::make(re, im);
             else Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, re, im);
         }
     }
@@ -202,8 +213,8 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
         for (int e = 0; e < R; ++e) {
             const int i = ib + e * 64 + lane;
-            const double2 v = stage[w0 * R + e * 64 + lane];
-            if (i < a.m) Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, v.x, v.y);
+            const SV v = stage[w0 * R + e * 64 + lane];
+            if (i < a.m) reinterpret_cast<SV *>(a.c)[(size_t)i + (size_t)j * a.ldc] = v;
         }
     }
 }
