@@ -52,10 +52,12 @@
  *       by the Cauchy-Schwarz inequality every |Re c|, |Im c| then stays
  *       recoverable.  Rows with a few dominant entries keep more bits than
  *       under the max rule.
- *     Entries are quantized as rint(a 2^(pA - E_i)), ties to even.  The
- *     result equals the exact integer product of the quantized operands
- *     rounded to nearest fp64 and scaled by 2^(E_i + F_j - pA - pB) (CGEMM:
- *     then rounded to fp32).
+ *     Entries are quantized as rint(a 2^(pA - E_i)), ties to even.  Each
+ *     output component equals the exact integer product of the quantized
+ *     operands times 2^(E_i + F_j - pA - pB), rounded ONCE to nearest (ties
+ *     to even) into the output type: fp64, or fp32 for CGEMM (never through
+ *     an fp64 rounding first), subnormal results included (Algorithm 1,
+ *     step 7).
  *   - Rows of A or columns of B containing Inf or NaN give NaN in the
  *     corresponding rows / columns of C; zero rows or columns give +0.
  *   - m == 0 or n == 0: nothing is done.  k == 0: C is set to zero.
@@ -119,7 +121,7 @@ o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double 
                     double *C, int ldc, int n_moduli, void *stream);
 
 /* C = A B in complex64: fp32 inputs are widened exactly, the same algorithm
-   runs, and the result is rounded to fp32 (Section 3.2; accuracy near fp32
+   runs, and the result is rounded once to fp32 (Section 3.2; accuracy near fp32
    needs about 8 moduli). */
 o2m_status cgemm_2m(int m, int n, int k, const float *A, int lda, const float *B, int ldb,
                     float *C, int ldc, int n_moduli, void *stream);

@@ -402,10 +402,12 @@ def lib():
         L.oracle_gauss_4m.argtypes = [I, I, I, P, I, P, I, P, I]
         L.oracle_gauss_4m.restype = I
         L.oracle_exponents.argtypes = [I, I, I, P, I, P, I, I, P, P, P, P]
-        L.oracle_oq_gemm.argtypes = [I, I, I, P, I, P, I, I, I, I, P, I, I, P, P]
+        L.oracle_oq_gemm.argtypes = [I, I, I, P, I, P, I, I, I, I, I, P, I, I, P, P]
         L.oracle_oq_cint.argtypes = [I, I, I, P, I, P, I, I, I, I, I, P, P, P]
         L.oracle_round_i128.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         L.oracle_round_i128.restype = ctypes.c_double
+        L.oracle_round_scaled.argtypes = [P, I, I]
+        L.oracle_round_scaled.restype = ctypes.c_double
         L.oracle_dd_gemm.argtypes = [I, I, I, P, I, P, I, P, P, I, I, P, P]
         _lib = L
     return _lib
@@ -475,18 +477,23 @@ def exponents(a: np.ndarray, b: np.ndarray, scaling: str = "max"):
 
 
 def oq_gemm_shifts(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries=None,
-                   scaling: str = "max") -> np.ndarray:
-    """Algorithm 1's exact output for given quantization shifts (C oracle)."""
+                   scaling: str = "max", out_dtype=np.complex128) -> np.ndarray:
+    """Algorithm 1's exact output for given quantization shifts (C oracle):
+    each component is the exact integer product, scaled, rounded once into
+    ``out_dtype`` (complex128 or complex64)."""
     a, b = _fortran_c128(a), _fortran_c128(b)
     m, k = a.shape
     k2, n = b.shape
     assert k == k2
+    f32 = np.dtype(out_dtype) == np.complex64
+    if not f32 and np.dtype(out_dtype) != np.complex128:
+        raise ValueError(f"unsupported output type {out_dtype}")
     ne, ei, ej = _entries(entries)
     if ne < 0:
-        C = np.zeros((m, n), dtype=np.complex128, order="F")
+        C = np.zeros((m, n), dtype=out_dtype, order="F")
     else:
-        C = np.zeros(ne, dtype=np.complex128)
-    lib().oracle_oq_gemm(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, _RULES[scaling], _ptr(C), m, ne,
+        C = np.zeros(ne, dtype=out_dtype)
+    lib().oracle_oq_gemm(m, n, k, _ptr(a), m, _ptr(b), k, pA, pB, _RULES[scaling], int(f32), _ptr(C), m, ne,
                          _ptr(ei), _ptr(ej))
     return C
 
@@ -499,10 +506,13 @@ def oq_zgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling:
 
 
 def oq_cgemm(a: np.ndarray, b: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
-    """CGEMM: fp32 inputs (exactly widened), the same algorithm, output rounded
-    to fp32 (round to nearest even)."""
-    out = oq_zgemm(a.astype(np.complex128), b.astype(np.complex128), n_moduli, entries, scaling)
-    return out.astype(np.complex64)
+    """CGEMM: fp32 inputs (exactly widened), the same algorithm, and step 7
+    rounds the exact scaled integer once to fp32 (nearest, ties to even), not
+    through an fp64 value first."""
+    a = np.asarray(a).astype(np.complex128)
+    b = np.asarray(b).astype(np.complex128)
+    pA, pB = shifts(scaling, moduli_set(n_moduli), a.shape[1])
+    return oq_gemm_shifts(a, b, pA, pB, entries, scaling, out_dtype=np.complex64)
 
 
 def oq_zherk(a: np.ndarray, n_moduli: int, entries=None, scaling: str = "max") -> np.ndarray:
@@ -574,6 +584,16 @@ def oq_cint(a: np.ndarray, b: np.ndarray, pA: int, pB: int, entries, scaling: st
             vals.append(v)
         res.append((vals[0], vals[1]))
     return res
+
+
+def round_scaled(v: int, scale: int, fmt: str = "f64") -> float:
+    """The C oracle's step-7 rounding of the integer v (|v| < 2^255) times
+    2^scale into fp64 or fp32 (``fmt``), returned as a Python float."""
+    if fmt not in ("f64", "f32"):
+        raise ValueError(fmt)
+    u = v & ((1 << 256) - 1)
+    w = np.array([(u >> (64 * t)) & ((1 << 64) - 1) for t in range(4)], dtype=np.uint64)
+    return lib().oracle_round_scaled(w.ctypes.data, scale, int(fmt == "f32"))
 
 
 def round_i128(v: int) -> float:

@@ -20,11 +20,13 @@
  *                   product C = A_int B_int exactly whenever every |Re c|,
  *                   |Im c| <= (M-1)/2 (Section 3.1), which the scaling budget
  *                   guarantees.  So Algorithm 1 returns
- *                     round_fp64(A_int B_int) * 2^(E_i + F_j - pA - pB)
+ *                     round(A_int B_int * 2^(E_i + F_j - pA - pB))
  *                   with A_int = round_Z(a * 2^(pA - E_i)) (step 3, componentwise,
  *                   ties to even), computed here in exact multiword integers
- *                   by 4M.  The moduli only enter through pA, pB, which the
- *                   caller derives from M (Python side).
+ *                   by 4M, and round() one rounding to nearest (ties to even)
+ *                   into the output format, fp64 or fp32, subnormals
+ *                   included (step 7).  The moduli only enter through pA,
+ *                   pB, which the caller derives from M (Python side).
  *
  *  oracle_dd_gemm   The product of the unquantized inputs by 4M in
  *                   double-double (error ~ k 2^-104 |A||B|): the reference the
@@ -82,8 +84,18 @@ static void acc_add_shifted(acc256 *a, i128 v, int shift) {
     }
 }
 
-/* Round a 256-bit signed integer to the nearest double, ties to even. */
-static double acc_to_double(const acc256 *a) {
+/* Bit b of the magnitude words w. */
+static int bit_of(const uint64_t w[4], int b) { return (int)((w[b >> 6] >> (b & 63)) & 1ULL); }
+
+/* Algorithm 1 step 7 for one component: the exact integer a times 2^scale,
+   rounded ONCE to the nearest value of a binary floating-point format with
+   `prec` significand bits and least normal exponent emin (fp64: 53, -1022;
+   fp32: 24, -126), ties to even, subnormal results included.  Values at or
+   beyond the format's largest finite magnitude after rounding become
+   infinities (for fp32 when the caller narrows the returned double, which
+   holds the rounded value exactly).  A zero integer gives +0; a negative value
+   that rounds to zero gives -0. */
+static double acc_round(const acc256 *a, int scale, int prec, int emin) {
     uint64_t w[4];
     memcpy(w, a->w, sizeof w);
     int neg = (int64_t)w[3] < 0;
@@ -99,27 +111,31 @@ static double acc_to_double(const acc256 *a) {
     for (int t = 3; t >= 0; --t)
         if (w[t]) { top = 64 * t + 63 - __builtin_clzll(w[t]); break; }
     if (top < 0) return 0.0;
+    /* the value lies in [2^e, 2^(e+1)); its quantum (the weight of the last
+       significand bit) is 2^(e - prec + 1), but never below the subnormal
+       quantum 2^(emin - prec + 1) */
+    int e = top + scale;
+    int qexp = e - prec + 1;
+    if (qexp < emin - prec + 1) qexp = emin - prec + 1;
+    int qpos = qexp - scale;                   /* bit of w with weight 2^qexp */
     double r;
-    if (top <= 52) {
-        r = (double)w[0];                      /* exact */
+    if (qpos <= 0) {
+        r = ldexp((double)w[0], scale);        /* fewer than prec bits: exact */
     } else {
-        int sh = top - 52;                     /* bits below the 53-bit mantissa */
-        /* mantissa = bits [sh, sh+52] */
+        /* significand = bits [qpos, top] (none when qpos > top) */
         uint64_t mant = 0;
-        for (int b = 0; b < 53; ++b) {
-            int bit = sh + b;
-            if ((w[bit >> 6] >> (bit & 63)) & 1ULL) mant |= 1ULL << b;
-        }
-        int rbit = sh - 1;
-        int round_bit = (int)((w[rbit >> 6] >> (rbit & 63)) & 1ULL);
+        for (int b = top; b >= qpos; --b) mant = (mant << 1) | (uint64_t)bit_of(w, b);
+        int round_bit = qpos - 1 <= top ? bit_of(w, qpos - 1) : 0;
         int sticky = 0;
-        for (int bit = 0; bit < rbit && !sticky; ++bit)
-            if ((w[bit >> 6] >> (bit & 63)) & 1ULL) sticky = 1;
-        if (round_bit && (sticky || (mant & 1ULL))) mant += 1; /* may reach 2^53: still exact */
-        r = ldexp((double)mant, sh);
+        for (int b = 0; b < qpos - 1 && b <= top; ++b)
+            if (bit_of(w, b)) { sticky = 1; break; }
+        if (round_bit && (sticky || (mant & 1ULL))) mant += 1; /* may reach 2^prec: still exact */
+        r = ldexp((double)mant, qexp);
     }
     return neg ? -r : r;
 }
+
+static double acc_to_double(const acc256 *a) { return acc_round(a, 0, 53, -1022); }
 
 static void acc_from_i128(acc256 *a, i128 v) {
     memset(a, 0, sizeof *a);
@@ -260,12 +276,13 @@ static void mul_acc(acc256 *acc, i128 *fast, int use_fast, qint x, qint y, int s
  * C (or the listed entries of C) = Algorithm 1 applied to A (m x k), B (k x n)
  * with quantization shifts pA, pB and exponent rule `rule`.  n_entries < 0: the full matrix into C with
  * leading dimension ldc.  n_entries >= 0: entry t = (ei[t], ej[t]) into
- * C[2t], C[2t+1].  Also returns, if c_int_out is non-null, the exact integer
- * products as doubles rounded (same as the unscaled output) -- used by tests.
+ * C[2t], C[2t+1].  out_f32 = 0: C is complex fp64 (double pairs); out_f32 = 1:
+ * C is complex fp32 (float pairs), each component the exact scaled integer
+ * rounded once to fp32 (CGEMM: never through an fp64 intermediate rounding).
  */
 void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
-                    int pA, int pB, int rule, double *C, int ldc, int n_entries, const int32_t *ei,
-                    const int32_t *ej) {
+                    int pA, int pB, int rule, int out_f32, void *C, int ldc, int n_entries,
+                    const int32_t *ei, const int32_t *ej) {
     int32_t *E = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *Eb = (int32_t *)malloc(sizeof(int32_t) * (m > 0 ? m : 1));
     int32_t *F = (int32_t *)malloc(sizeof(int32_t) * (n > 0 ? n : 1));
@@ -289,8 +306,14 @@ void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double 
             int i, j;
             if (n_entries < 0) { j = (int)(t / m); i = (int)(t % m); }
             else { i = ei[t]; j = ej[t]; }
-            double *out = n_entries < 0 ? C + 2 * ((long)i + (long)j * ldc) : C + 2 * t;
-            if (Eb[i] || Fb[j]) { out[0] = NAN; out[1] = NAN; continue; }
+            const long o = n_entries < 0 ? 2 * ((long)i + (long)j * ldc) : 2 * t;
+            double *out64 = (double *)C + o;
+            float *out32 = (float *)C + o;
+            if (Eb[i] || Fb[j]) {
+                if (out_f32) { out32[0] = NAN; out32[1] = NAN; }
+                else { out64[0] = NAN; out64[1] = NAN; }
+                continue;
+            }
             if (j != cached_j) {
                 for (int p = 0; p < k; ++p)
                     quantize(B + 2 * ((long)p + (long)j * ldb), pB - F[j], &bre[p], &bim[p]);
@@ -310,9 +333,15 @@ void oracle_oq_gemm(int m, int n, int k, const double *A, int lda, const double 
                 mul_acc(&im, &fim, use_fast, aim, bre[p], +1);
             }
             if (use_fast) { acc_from_i128(&re, fre); acc_from_i128(&im, fim); }
+            /* step 7: one rounding of c_int 2^(E_i + F_j - pA - pB) */
             int scale = E[i] + F[j] - pA - pB;
-            out[0] = ldexp(acc_to_double(&re), scale);
-            out[1] = ldexp(acc_to_double(&im), scale);
+            if (out_f32) {
+                out32[0] = (float)acc_round(&re, scale, 24, -126);  /* exact narrowing */
+                out32[1] = (float)acc_round(&im, scale, 24, -126);
+            } else {
+                out64[0] = acc_round(&re, scale, 53, -1022);
+                out64[1] = acc_round(&im, scale, 53, -1022);
+            }
         }
         free(bre);
         free(bim);
@@ -359,6 +388,14 @@ double oracle_round_i128(uint64_t lo, uint64_t hi) {
     i128 v = (i128)(((u128)hi << 64) | lo);
     acc_from_i128(&a, v);
     return acc_to_double(&a);
+}
+
+/* The step-7 rounding of a 256-bit signed integer w (little-endian words)
+   times 2^scale into fp64 (f32 = 0) or fp32 (f32 = 1), for pins. */
+double oracle_round_scaled(const uint64_t *w, int scale, int f32) {
+    acc256 a;
+    memcpy(a.w, w, sizeof a.w);
+    return f32 ? acc_round(&a, scale, 24, -126) : acc_round(&a, scale, 53, -1022);
 }
 
 /* ------------------------------------------------------------------------ */

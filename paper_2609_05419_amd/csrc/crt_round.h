@@ -83,9 +83,28 @@ O2M_HD inline void add_shifted(UW<W> &a, int64_t x, int s) {
 
 O2M_HD inline int clz64(uint64_t x) { return __builtin_clzll(x); }
 
-// RN of a W-word signed integer, ties to even, times 2^sc (one rounding).
-template <int W>
-O2M_HD inline double round_words(UW<W> v, int sc) {
+// x + y + z rounded to odd (the same TwoSum cascade as sum3_rn with the last
+// addition rounded to odd too).  The inner round-to-odd sum v of the two error
+// terms has a last significand bit of 1 unless it is exact, so it is never a
+// point of the outer sum's grid (multiples of half an ulp of th, all of them
+// representable at v's smaller scale with an even last bit); th + v and the
+// exact sum therefore lie strictly between the same two neighbouring doubles,
+// or are both exact, and round to odd alike.
+O2M_HD inline double sum3_ro(double a, double b, double c) {
+    double uh, ul, th, tl;
+    two_sum(b, c, uh, ul);
+    two_sum(a, uh, th, tl);
+    return sum_round_odd(th, sum_round_odd(tl, ul));
+}
+
+// The integer v of W words times 2^sc, rounded once to nearest (ties to even)
+// into a binary format with P significand bits and least normal exponent EMIN
+// (fp64: 53, -1022; fp32: 24, -126), subnormal results included.  The result
+// is returned as a double holding the rounded value exactly (for fp32 it then
+// narrows to float without a second rounding, or to an infinity beyond the
+// fp32 range).  Zero gives +0; a negative value that rounds to zero gives -0.
+template <int W, int P, int EMIN>
+O2M_HD inline double round_words_fmt(UW<W> v, int sc) {
     const bool neg = (int64_t)v.w[W - 1] < 0;
     if (neg) {
         uint64_t carry = 1;
@@ -118,12 +137,30 @@ O2M_HD inline double round_words(UW<W> v, int sc) {
     uint64_t h = hi << lz;
     if (lz) h |= lo >> (64 - lz);
     const uint64_t rest = (lo << lz) | low;
-    uint64_t mant = h >> 11;
-    const uint64_t rb = h & 0x7FF;
-    if (rb > 0x400 || (rb == 0x400 && (rest != 0 || (mant & 1)))) mant += 1;
-    const int msb = 64 * top + 63 - lz;  // bit index of the leading one
-    const double r = ldexp((double)mant, msb - 52 + sc);
+    const int e = 64 * top + 63 - lz + sc;   // the value lies in [2^e, 2^(e+1))
+    // significand bits kept: P, fewer for a subnormal result
+    const int keep = e >= EMIN ? P : P - (EMIN - e);
+    double r;
+    if (keep <= 0) {
+        // below the least subnormal q = 2^(EMIN - P + 1): the value is in
+        // [q/2, q) when keep == 0 (up unless exactly q/2, a tie to 0), else
+        // below q/2
+        r = keep == 0 && ((h << 1) != 0 || rest != 0) ? ldexp(1.0, EMIN - P + 1) : 0.0;
+    } else {
+        uint64_t mant = h >> (64 - keep);
+        const uint64_t below = h << keep;   // the dropped bits of h, left aligned
+        const bool half = (below >> 63) != 0;
+        const bool sticky = (below << 1) != 0 || rest != 0;
+        if (half && (sticky || (mant & 1))) mant += 1;  // may reach 2^keep: still exact
+        r = ldexp((double)mant, e - keep + 1);
+    }
     return neg ? -r : r;
+}
+
+// RN to fp64 of a W-word signed integer times 2^sc (one rounding).
+template <int W>
+O2M_HD inline double round_words(UW<W> v, int sc) {
+    return round_words_fmt<W, 53, -1022>(v, sc);
 }
 
 // Words needed for T limbs of 40 bits with |c_t| < 2^53, plus the sign.
@@ -132,28 +169,69 @@ struct LimbWords {
     static constexpr int value = (40 * (T - 1) + 54 + 63) / 64;
 };
 
-// Steps 5-7 for one component: limb sums S_t = sum_l u_l w_lt (exact), the
-// quotient q = rint(X / M) from a fp64 Horner sum (exact while |c| / M stays
-// below 1/2 - 2^-32), the lifted limbs c_t = S_t - q M_t (exact), and
-// RN(c) * 2^sc.  T <= 3 rounds with the three-term sum; T >= 4 through a
-// multiword integer (192 bits for T = 4, 256 bits for T = 5, 6).
+// Step 6 for one component: the quotient q = rint(X / M) from a fp64 Horner
+// sum of the limb sums S_t (exact while |c| / M stays below 1/2 - 2^-32) and
+// the lifted limbs c_t = S_t - q M_t (exact).
 template <int T>
-O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
+O2M_HD inline void lift_limbs(const double (&S)[T], const double *mlimb, double inv_m, double (&c)[T]) {
     double X = S[T - 1];
     for (int t = T - 2; t >= 0; --t) X = fma(X, kTwo40, S[t]);
     const double q = rint(X * inv_m);
-    double c[T];
     for (int t = 0; t < T; ++t) c[t] = fma(-q, mlimb[t], S[t]);
-    if constexpr (T == 2) {
-        return ldexp(fma(c[1], kTwo40, c[0]), sc);              // one rounding of an exact sum
-    } else if constexpr (T == 3) {
-        return ldexp(sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]), sc);
-    } else {
-        constexpr int W = LimbWords<T>::value;
-        UW<W> v = {};
+}
+
+// The lifted limbs as one multiword integer.
+template <int T>
+O2M_HD inline UW<LimbWords<T>::value> words_of(const double (&c)[T]) {
+    constexpr int W = LimbWords<T>::value;
+    UW<W> v = {};
 #pragma unroll
-        for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)c[t], 40 * t);
-        return round_words<W>(v, sc);
+    for (int t = 0; t < T; ++t) add_shifted<W>(v, (int64_t)c[t], 40 * t);
+    return v;
+}
+
+// Steps 5-7 for one component with fp64 output: the lifted limbs, then
+// RN(c 2^sc), one rounding.  T <= 3 rounds c with the exact limb sum (T = 2)
+// or the three-term sum and scales by 2^sc, which is exact unless the result
+// is subnormal; such results (and those that underflow to zero) are rounded
+// again from the exact integer at the subnormal quantum.  T >= 4 rounds
+// through a multiword integer (192 bits for T = 4, 256 bits for T = 5, 6).
+template <int T>
+O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
+    double c[T];
+    lift_limbs<T>(S, mlimb, inv_m, c);
+    if constexpr (T <= 3) {
+        double x;
+        if constexpr (T == 2) x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
+        else x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        const double r = ldexp(x, sc);
+        if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
+        return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
+    } else {
+        return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
+    }
+}
+
+// Steps 5-7 with fp32 output (CGEMM): RN32(c 2^sc), one rounding.  For T <= 3
+// the limb sum is rounded to odd in fp64 and then to fp32: a value rounded to
+// odd with 53 >= 24 + 2 bits rounds to nearest exactly as the exact value
+// does, in the normal and subnormal fp32 ranges alike, as long as the scaling
+// by 2^sc is exact in fp64 (true unless the fp64 value is subnormal, which
+// takes the multiword path).  T >= 4 rounds the multiword integer to 24 bits
+// directly.
+template <int T>
+O2M_HD inline float lift_round_f32(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
+    double c[T];
+    lift_limbs<T>(S, mlimb, inv_m, c);
+    if constexpr (T <= 3) {
+        double x;
+        if constexpr (T == 2) x = sum_round_odd(c[1] * kTwo40, c[0]);
+        else x = sum3_ro(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        const double r = ldexp(x, sc);
+        if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return (float)r;
+        return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
+    } else {
+        return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
     }
 }
 

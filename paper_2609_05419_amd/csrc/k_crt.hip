@@ -12,9 +12,11 @@
 // q = rint(X / M) is estimated from a fp64 Horner sum; the scaling budget keeps
 // |c| / M <= 1/2 - 2^-32, far from the rounding boundary, so q is exact.  The
 // lifted value c = X - q M (step 6) is then exact as limbs c_t = S_t - q M_t,
-// rounded to the nearest double, ties to even (a correctly rounded three-term
-// sum for T <= 3 limbs, a 192- or 256-bit integer for T = 4..6: crt_round.h),
-// and scaled by 2^(E_i + F_j - pA - pB) (step 7).
+// and step 7 rounds c 2^(E_i + F_j - pA - pB) once, to nearest with ties to
+// even, into the output type (fp64: a correctly rounded limb sum, or a 192- or
+// 256-bit integer for T = 4..6, with subnormal results rounded from the exact
+// integer; fp32: the limb sum rounded to odd in fp64, then to fp32:
+// crt_round.h).
 //
 // Hybrid sets (Section 3.2): for the 3M moduli the GEMM left T1 = Ar Br,
 // T2 = Ai Bi, T3 = (Ar + Ai)(Br + Bi) mod m, so u = T1 - T2 and
@@ -33,28 +35,25 @@ namespace {
 
 __device__ inline int sext8(uint32_t w, int e) { return (int)(int8_t)(w >> (8 * e)); }
 
-template <ElemType OT> struct Out;
-template <> struct Out<kF64> {
-    static __device__ inline void put(void *c, size_t idx, double re, double im) {
-        reinterpret_cast<double2 *>(c)[idx] = make_double2(re, im);
-    }
-};
-template <> struct Out<kF32> {
-    static __device__ inline void put(void *c, size_t idx, double re, double im) {
-        reinterpret_cast<float2 *>(c)[idx] = make_float2((float)re, (float)im);
-    }
-};
+// One output entry in its stored type.
+template <ElemType OT> struct OutT { typedef double2 type; };
+template <> struct OutT<kF32> { typedef float2 type; };
 
-// An output entry as staged in LDS: the stored type itself.
-template <ElemType OT> struct Staged;
-template <> struct Staged<kF64> {
-    typedef double2 type;
-    static __device__ inline type make(double re, double im) { return make_double2(re, im); }
-};
-template <> struct Staged<kF32> {
-    typedef float2 type;
-    static __device__ inline type make(double re, double im) { return make_float2((float)re, (float)im); }
-};
+// Step 7 for both components of one entry: RN(c 2^sc) into the output type,
+// one rounding (fp32: never through an fp64 rounding first); NaN for a
+// non-finite row or column.
+template <int T, ElemType OT>
+__device__ inline typename OutT<OT>::type finish(const double (&sre)[T], const double (&sim)[T],
+                                                 const CrtParams &cp, bool bad, int sc) {
+    if constexpr (OT == kF32) {
+        if (bad) return make_float2(__builtin_nanf(""), __builtin_nanf(""));
+        return make_float2(lift_round_f32<T>(sre, cp.mlimb, cp.inv_m, sc),
+                           lift_round_f32<T>(sim, cp.mlimb, cp.inv_m, sc));
+    } else {
+        if (bad) return make_double2(__builtin_nan(""), __builtin_nan(""));
+        return make_double2(lift_round<T>(sre, cp.mlimb, cp.inv_m, sc), lift_round<T>(sim, cp.mlimb, cp.inv_m, sc));
+    }
+}
 
 // MODE 0: ZGEMM / CGEMM output.  MODE 3: exact Gaussian integers (int64).
 // MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R = 4
@@ -71,7 +70,7 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
     // lane: a wave leaves only when all its rows are beyond m, and a lane
     // beyond m reads row 0 instead (its sums are never stored)
     constexpr bool STAGE = MODE == 0;
-    typedef typename Staged<OT == kF32 ? kF32 : kF64>::type SV;
+    typedef typename OutT<OT>::type SV;
     __shared__ SV stage[STAGE ? 256 * R : 1];
     const int lane = threadIdx.x & 63, w0 = threadIdx.x & ~63;
     if ((STAGE ? i0 - lane * R : i0) >= a.m) return;
@@ -192,17 +191,9 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
             if (need > (unsigned __int128)(uint64_t)h) atomicOr(a.status, kStatusOverflow);
         } else {
             const int ei = a.E[i], fj = a.F[j];
-            double re, im;
-            if (ei == INT32_MIN || fj == INT32_MIN) {
-                re = __builtin_nan("");
-                im = re;
-            } else {
-                const int sc = ei + fj + a.scale_bias;
-                re = lift_round<T>(sre[e], cp.mlimb, cp.inv_m, sc);
-                im = lift_round<T>(sim[e], cp.mlimb, cp.inv_m, sc);
-            }
-            if constexpr (STAGE) stage[threadIdx.x * R + e] = Staged<OT == kF32 ? kF32 : kF64>::make(re, im);
-            else Out<OT>::put(a.c, (size_t)i + (size_t)j * a.ldc, re, im);
+            const SV v = finish<T, OT>(sre[e], sim[e], cp, ei == INT32_MIN || fj == INT32_MIN, ei + fj + a.scale_bias);
+            if constexpr (STAGE) stage[threadIdx.x * R + e] = v;
+            else reinterpret_cast<SV *>(a.c)[(size_t)i + (size_t)j * a.ldc] = v;
         }
     }
     if constexpr (STAGE) {

@@ -4,15 +4,28 @@
 
 namespace {
 template <int T>
-double lift(const double *S, const double *mlimb, double inv_m, int sc) {
+double lift(const double *S, const double *mlimb, double inv_m, int sc, int f32) {
     double s[T];
     for (int t = 0; t < T; ++t) s[t] = S[t];
-    return o2m::lift_round<T>(s, mlimb, inv_m, sc);
+    return f32 ? (double)o2m::lift_round_f32<T>(s, mlimb, inv_m, sc) : o2m::lift_round<T>(s, mlimb, inv_m, sc);
+}
+
+template <int W>
+double round_fmt(const int64_t *limbs, int T, int sc, int f32) {
+    o2m::UW<W> v = {};
+    for (int t = 0; t < T; ++t) o2m::add_shifted<W>(v, limbs[t], 40 * t);
+    return f32 ? o2m::round_words_fmt<W, 24, -126>(v, sc) : o2m::round_words_fmt<W, 53, -1022>(v, sc);
 }
 }  // namespace
 
 extern "C" {
 double t_sum3_rn(double a, double b, double c) { return o2m::sum3_rn(a, b, c); }
+double t_sum3_ro(double a, double b, double c) { return o2m::sum3_ro(a, b, c); }
+double t_sum_ro(double a, double b) { return o2m::sum_round_odd(a, b); }
+// T limbs (T <= 6) rounded into fp64 (f32 = 0) or fp32 (f32 = 1) after 2^sc
+double t_round_limbs_fmt(const int64_t *limbs, int T, int sc, int f32) {
+    return T <= 4 ? round_fmt<3>(limbs, T, sc, f32) : round_fmt<4>(limbs, T, sc, f32);
+}
 double t_round_limbs(const int64_t *limbs, int T, int sc) {
     if (T <= 4) {
         o2m::UW<3> v = {};
@@ -23,13 +36,13 @@ double t_round_limbs(const int64_t *limbs, int T, int sc) {
     for (int t = 0; t < T; ++t) o2m::add_shifted<4>(v, limbs[t], 40 * t);
     return o2m::round_words<4>(v, sc);
 }
-double t_lift_round(const double *S, int T, const double *mlimb, double inv_m, int sc) {
+double t_lift_round(const double *S, int T, const double *mlimb, double inv_m, int sc, int f32) {
     switch (T) {
-    case 2: return lift<2>(S, mlimb, inv_m, sc);
-    case 3: return lift<3>(S, mlimb, inv_m, sc);
-    case 4: return lift<4>(S, mlimb, inv_m, sc);
-    case 5: return lift<5>(S, mlimb, inv_m, sc);
-    default: return lift<6>(S, mlimb, inv_m, sc);
+    case 2: return lift<2>(S, mlimb, inv_m, sc, f32);
+    case 3: return lift<3>(S, mlimb, inv_m, sc, f32);
+    case 4: return lift<4>(S, mlimb, inv_m, sc, f32);
+    case 5: return lift<5>(S, mlimb, inv_m, sc, f32);
+    default: return lift<6>(S, mlimb, inv_m, sc, f32);
     }
 }
 }

@@ -1,7 +1,8 @@
 """Host build of the CRT kernel's rounding (crt_round.h) against Python's
-correctly rounded int -> float conversion: the three-term round-to-odd sum, the
-multiword paths (192 and 256 bits), and the full lift with real CRT tables
-built by the oracle (2M and hybrid sets)."""
+correctly rounded int -> float conversion and the oracle's pinned step-7
+rounding: the three-term sums (to nearest and to odd), the multiword paths
+(192 and 256 bits) into fp64 and fp32 with subnormal results, and the full
+lift with real CRT tables built by the oracle (2M and hybrid sets)."""
 import ctypes
 import math
 import os
@@ -27,9 +28,39 @@ def lib(tmp_path_factory):
     L.t_sum3_rn.restype = D
     L.t_round_limbs.argtypes = [P, I, I]
     L.t_round_limbs.restype = D
-    L.t_lift_round.argtypes = [P, I, P, D, I]
+    L.t_lift_round.argtypes = [P, I, P, D, I, I]
     L.t_lift_round.restype = D
+    L.t_sum3_ro.argtypes = [D, D, D]
+    L.t_sum3_ro.restype = D
+    L.t_sum_ro.argtypes = [D, D]
+    L.t_sum_ro.restype = D
+    L.t_round_limbs_fmt.argtypes = [P, I, I, I]
+    L.t_round_limbs_fmt.restype = D
     return L
+
+
+def narrow(x: float, fmt: str) -> float:
+    """The oracle's fp32 rounding returns the rounded value as a double; the
+    kernel's fp32 result is that value narrowed (infinite beyond fp32's range)."""
+    if fmt == "f64":
+        return x
+    with np.errstate(over="ignore"):
+        return float(np.float32(x))
+
+
+def round_odd(c: int) -> float:
+    """c rounded to odd with 53 bits: truncated toward zero, last bit forced
+    to 1 when anything was cut off."""
+    a = abs(c)
+    n = a.bit_length()
+    if n <= 53:
+        return float(c)
+    sh = n - 53
+    mant = a >> sh
+    if a & ((1 << sh) - 1):
+        mant |= 1
+    r = float(mant << sh)
+    return -r if c < 0 else r
 
 
 def split_limbs(c: int, T: int, rng: random.Random):
@@ -71,6 +102,43 @@ def test_three_term_sum_is_correctly_rounded(lib):
         assert got == float(c), c
 
 
+def test_three_term_sum_rounds_to_odd(lib):
+    rng = random.Random(4)
+    vals = interesting_integers(rng, 119)
+    for _ in range(3000):   # 24-bit ties (the fp32 case) and their neighbours
+        s = rng.randint(2, 119 - 25)
+        m = rng.randint(1 << 23, (1 << 24) - 1)
+        v = (m << s) + (1 << (s - 1)) + rng.choice((-1, 0, 1))
+        vals.append(v if rng.random() < 0.5 else -v)
+    for c in vals:
+        c0, c1, c2 = split_limbs(c, 3, rng)
+        got = lib.t_sum3_ro(float(c2) * 2.0 ** 80, float(c1) * 2.0 ** 40, float(c0))
+        assert got == round_odd(c), c
+        c0, c1 = split_limbs(c >> 40, 2, rng) if abs(c) < 1 << 90 else (0, 0)
+        if abs(c) < 1 << 90:
+            cc = c >> 40
+            got = lib.t_sum_ro(float(c1) * 2.0 ** 40, float(c0))
+            assert got == round_odd(cc), cc
+
+
+@pytest.mark.parametrize("T,bits", [(2, 90), (3, 130), (4, 150), (5, 190), (6, 245)])
+@pytest.mark.parametrize("fmt", ["f64", "f32"])
+def test_multiword_rounding_into_format(lib, T, bits, fmt):
+    """One rounding of c 2^sc into fp64 / fp32, subnormal results included,
+    equals the oracle's pinned step-7 rounding."""
+    rng = random.Random(10 * T + (fmt == "f32"))
+    emin, prec = (-1022, 53) if fmt == "f64" else (-126, 24)
+    for c in interesting_integers(rng, bits)[:2500]:
+        limbs = split_limbs(c, T, rng)
+        arr = np.array(limbs, dtype=np.int64)
+        n = abs(c).bit_length()
+        # normal, subnormal (quantum anywhere in c), and below half the least subnormal
+        for sc in (rng.randint(-60, 60), emin - prec + 1 - rng.randint(0, n + 1), emin - n - rng.randint(0, 3)):
+            got = narrow(lib.t_round_limbs_fmt(arr.ctypes.data, T, sc, int(fmt == "f32")), fmt)
+            want = narrow(O.round_scaled(c, sc, fmt), fmt)
+            assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, sc, got, want)
+
+
 @pytest.mark.parametrize("T,bits", [(4, 150), (5, 190), (6, 245)])
 def test_multiword_rounding(lib, T, bits):
     rng = random.Random(T)
@@ -83,12 +151,14 @@ def test_multiword_rounding(lib, T, bits):
 
 
 @pytest.mark.parametrize("N", [4, 8, 12, 16, 17, 22, 23, 27, 28, 32])
-def test_lift_round_with_crt_tables(lib, N):
+@pytest.mark.parametrize("fmt", ["f64", "f32"])
+def test_lift_round_with_crt_tables(lib, N, fmt):
     """Limb sums built the way the CRT kernel builds them (balanced base-2^40
     weights folded with 2^-1; plain weights for the 3M moduli of a hybrid set),
-    lifted and rounded, equal RN of the exact symmetric lift computed with
-    Python integers."""
-    rng = random.Random(N)
+    lifted and rounded once into fp64 or fp32 (normal and subnormal results),
+    equal the oracle's step-7 rounding of the exact symmetric lift computed
+    with Python integers."""
+    rng = random.Random(N + 100 * (fmt == "f32"))
     ms = O.moduli_set(N)
     M = O.product(ms)
     T = max(2, math.ceil((math.log2(M) + 1) / 40))
@@ -116,8 +186,15 @@ def test_lift_round_with_crt_tables(lib, N):
     h = (M - 1) // 2
     bound = h - (M >> 32)
     inv_m = 1.0 / float(M)
-    for _ in range(400):
+    emin, prec = (-1022, 53) if fmt == "f64" else (-126, 24)
+    for it in range(600):
         c = rng.randint(-bound, bound)
+        ps = [p for p in (24, 53) if bound.bit_length() - p - 2 >= 2]
+        if it % 3 == 1 and ps:   # a tie of the output format's significand, +-1
+            p = rng.choice(ps)
+            s = rng.randint(2, bound.bit_length() - p - 2)
+            c = (rng.randint(1 << (p - 1), (1 << p) - 1) << s) + (1 << (s - 1)) + rng.choice((-1, 0, 1))
+            c = c if rng.random() < 0.5 else -c
         # residues of c mod each m, split as u = r- + r+ with symmetric parts
         u = []
         for q in ms:
@@ -138,6 +215,8 @@ def test_lift_round_with_crt_tables(lib, N):
                 u.append(t1 - t2)
         S = np.array([sum(u[l] * wl[l][t] for l in range(N)) for t in range(T)], dtype=np.float64)
         assert all(abs(sum(u[l] * wl[l][t] for l in range(N))) < 1 << 53 for t in range(T))
-        sc = rng.randint(-60, 60)
-        got = lib.t_lift_round(S.ctypes.data, T, ml.ctypes.data, inv_m, sc)
-        assert got == math.ldexp(float(c), sc), (N, c)
+        n = abs(c).bit_length()
+        sc = rng.randint(-60, 60) if it % 2 == 0 else emin - prec + 1 - rng.randint(0, n + 1)
+        got = lib.t_lift_round(S.ctypes.data, T, ml.ctypes.data, inv_m, sc, int(fmt == "f32"))
+        want = narrow(O.round_scaled(c, sc, fmt), fmt)
+        assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (N, c, sc)

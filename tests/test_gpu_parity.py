@@ -1,7 +1,7 @@
 """Parity of the HIP path (through the C-ABI) with the CPU oracle.
 
 Floating-point results are compared bit for bit with the oracle's exact output
-of Algorithm 1 (the quantized product, rounded to nearest fp64, rescaled):
+of Algorithm 1 (the quantized product, rescaled, rounded once to the output type):
 the GPU path computes that same number exactly, so any difference is a bug.
 Accuracy against the unquantized product (double-double reference) is checked
 separately with the tolerance 4 u k |A||B| (u = 2^-53 for ZGEMM, 2^-24 for

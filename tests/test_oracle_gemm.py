@@ -188,16 +188,6 @@ def test_herk_and_syrk_oracles():
         assert np.array_equal(c, tiny.real)
 
 
-def test_cgemm_oracle_rounds_to_fp32():
-    rng = np.random.default_rng(13)
-    a = np.asfortranarray(rand_complex(rng, 4, 5).astype(np.complex64))
-    b = np.asfortranarray(rand_complex(rng, 5, 3).astype(np.complex64))
-    c = O.oq_cgemm(a, b, 8)
-    assert c.dtype == np.complex64
-    wide = O.oq_zgemm(a.astype(np.complex128), b.astype(np.complex128), 8)
-    assert np.array_equal(c, wide.astype(np.complex64))
-
-
 # --------------------------------------------------------------- O-F
 
 
