@@ -63,18 +63,25 @@
  *   - m == 0 or n == 0: nothing is done.  k == 0: C is set to zero.
  *
  * Workspace: the library needs device scratch memory for the residue planes
- * (size: o2m_workspace_bytes).  It allocates it on first use per device and
- * grows it as needed (hipMalloc, synchronizing the device when it grows); a
- * caller may instead hand over its own buffer with o2m_set_workspace.
- * Calls on one device share that workspace: calls that overlap in time on
- * different streams of the same device race.
+ * (size: o2m_workspace_bytes).  Each stream of each device has its own: calls
+ * on one stream run in order and share it, calls on different streams never
+ * share scratch memory, so they may overlap in time.  The library allocates a
+ * stream's workspace on its first call and grows it as needed (hipMalloc,
+ * after synchronizing that stream); o2m_release_workspace frees it.  A caller
+ * may instead bind its own buffer to a stream with o2m_set_workspace.  A
+ * workspace is keyed by the stream handle: a stream destroyed while its calls
+ * still run must not be replaced by a new stream with the same handle before
+ * they finish.
  *
- * Graph capture: once the workspace is large enough for a call (an earlier
- * call of the same or a larger size, or o2m_set_workspace), the call enqueues
- * kernels only (no allocation, no host synchronisation, no memset: buffers
- * are cleared by kernels), so it can be captured into a HIP graph on its
- * stream and replayed; each replay reads the captured input buffers anew.
- * With phase timing on, the captured call records its events as well.
+ * Graph capture: once the workspace of the capturing stream is large enough
+ * for a call (an earlier call of the same or a larger size on that stream, or
+ * o2m_set_workspace for it), the call enqueues kernels only (no allocation,
+ * no host synchronisation, no memset: buffers are cleared by kernels), so it
+ * can be captured into a HIP graph on its stream and replayed; each replay
+ * reads the captured input buffers anew.  A call under capture that would
+ * need a larger workspace fails with O2M_ERR_WORKSPACE and leaves the capture
+ * intact.  With phase timing on, the captured call records its events as
+ * well.
  *
  * Return value: O2M_OK, or a negative code.  -1 .. -12: the position of the
  * first invalid argument (BLAS convention, counting from 1).  Errors found
@@ -97,7 +104,9 @@ typedef int o2m_status;
                                    calls), 1..8 (gauss mode)                        */
 #define O2M_ERR_KLIMIT (-21)    /* k > 149130 (131071 when N > 22): int32
                                    accumulation could overflow                      */
-#define O2M_ERR_WORKSPACE (-22) /* caller workspace too small                       */
+#define O2M_ERR_WORKSPACE (-22) /* workspace too small: a caller buffer, or a stream
+                                   under graph capture whose workspace was not
+                                   sized before the capture                        */
 #define O2M_ERR_HIP (-23)       /* a HIP runtime call or kernel launch failed       */
 #define O2M_ERR_NOMEM (-24)     /* workspace allocation failed                      */
 #define O2M_ERR_SIZE (-25)      /* a padded size or plane offset exceeds the range  */
@@ -110,6 +119,9 @@ typedef int o2m_status;
 
 /* device status bits, read with o2m_get_status */
 #define O2M_STATUS_OVERFLOW 1   /* gauss mode: 2k max|A_i| max|B_j| > (M-1)/2    */
+#define O2M_STATUS_NONFINITE 2  /* a row of A or column of B held Inf or NaN (its
+                                   row / column of C is NaN); Algorithm 1 is
+                                   silent on non-finite inputs                    */
 
 #define O2M_MAX_MODULI 22          /* 2M moduli (Section 4)                        */
 #define O2M_MAX_MODULI_HYBRID 32   /* GEMM calls with the 3M extension (Section 3.2) */
@@ -213,13 +225,20 @@ o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, in
    Touches no GPU. */
 size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli);
 
-/* Use caller-owned device memory (on the current device) as the workspace
-   from now on; NULL returns to library-managed memory.  The caller keeps
-   ownership and must keep it alive while calls using it may still run. */
-o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes);
+/* Use caller-owned device memory (on the current device) as the workspace of
+   the calls on `stream` from now on; NULL returns that stream to
+   library-managed memory.  The caller keeps ownership and must keep the
+   buffer alive while calls using it may still run.  Calls whose workspace
+   exceeds `bytes` fail with O2M_ERR_WORKSPACE. */
+o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes, void *stream);
 
-/* Synchronize stream, return the device status bits of the current device
-   in *device_status and clear them. */
+/* Free the library-owned workspace of `stream` on the current device, after
+   synchronizing that stream (the next call on it allocates anew). */
+o2m_status o2m_release_workspace(void *stream);
+
+/* Synchronize stream, return the device status bits of the current device in
+   *device_status and clear them.  The bits are shared by the device's
+   streams: they are the OR over every call since the last read. */
 o2m_status o2m_get_status(void *stream, int *device_status);
 
 /* Phase timing for profiling: when enabled (which also restarts the count),

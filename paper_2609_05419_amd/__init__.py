@@ -20,7 +20,7 @@ import torch
 __all__ = [
     "zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
     "zgemm_2m_residues", "moduli", "budget", "shifts", "workspace_bytes", "set_workspace",
-    "get_status", "phase_timing", "phase_times", "colmajor", "O2MError", "LIB_PATH", "SCALING",
+    "release_workspace", "get_status", "STATUS_OVERFLOW", "STATUS_NONFINITE", "phase_timing", "phase_times", "colmajor", "O2MError", "LIB_PATH", "SCALING",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libo2m.so")
@@ -50,7 +50,8 @@ _L.o2m_budget.argtypes = [_I, _I, _P]
 _L.o2m_shifts.argtypes = [_C, _I, _I, _I, _P, _P]
 _L.o2m_workspace_bytes.argtypes = [ctypes.c_char, _I, _I, _I, _I]
 _L.o2m_workspace_bytes.restype = ctypes.c_size_t
-_L.o2m_set_workspace.argtypes = [_P, ctypes.c_size_t]
+_L.o2m_set_workspace.argtypes = [_P, ctypes.c_size_t, _P]
+_L.o2m_release_workspace.argtypes = [_P]
 _L.o2m_get_status.argtypes = [_P, _P]
 _L.o2m_phase_timing.argtypes = [_I]
 _L.o2m_phase_times.argtypes = [_P, _I]
@@ -59,10 +60,12 @@ _L.o2m_status_string.restype = ctypes.c_char_p
 for _f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex",
            "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex", "zher2k_2m_ex", "dsyr2k_2m_ex", "gauss_gemm_2m",
            "zgemm_2m_residues", "zgemm_2m_residues_ex", "o2m_moduli", "o2m_budget", "o2m_shifts",
-           "o2m_set_workspace", "o2m_get_status", "o2m_phase_timing", "o2m_phase_times"):
+           "o2m_set_workspace", "o2m_release_workspace", "o2m_get_status", "o2m_phase_timing",
+           "o2m_phase_times"):
     getattr(_L, _f).restype = _I
 
 STATUS_OVERFLOW = 1
+STATUS_NONFINITE = 2
 # scaling rules: "max" (per-row maximum) and "cs" (Cauchy-Schwarz, 2-norm)
 SCALING = {"max": 0, "cs": 1}
 
@@ -267,11 +270,33 @@ def workspace_bytes(op: str, m: int, n: int, k: int, n_moduli: int) -> int:
     return int(_L.o2m_workspace_bytes(op.encode()[:1], m, n, k, n_moduli))
 
 
-def set_workspace(buf: torch.Tensor | None) -> None:
+# caller workspaces bound to (device, stream): held here so that their memory
+# stays allocated while the library may write into it
+_workspaces: dict = {}
+
+
+def set_workspace(buf: torch.Tensor | None, stream=None) -> None:
+    """Bind a caller-owned device buffer (contiguous, on the current device) as
+    the workspace of the calls on ``stream`` (default: the current stream);
+    None returns the stream to library-managed memory.  The binding keeps a
+    reference to ``buf`` until it is replaced or cleared."""
+    dev = torch.cuda.current_device()
+    handle = _stream(stream)
     if buf is None:
-        _check(_L.o2m_set_workspace(None, 0), "o2m_set_workspace")
-    else:
-        _check(_L.o2m_set_workspace(buf.data_ptr(), buf.numel() * buf.element_size()), "o2m_set_workspace")
+        _check(_L.o2m_set_workspace(None, 0, handle), "o2m_set_workspace")
+        _workspaces.pop((dev, handle), None)
+        return
+    if not buf.is_cuda or buf.device.index != dev:
+        raise ValueError(f"workspace must be a tensor on the current device cuda:{dev}")
+    if not buf.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    _check(_L.o2m_set_workspace(buf.data_ptr(), buf.numel() * buf.element_size(), handle), "o2m_set_workspace")
+    _workspaces[(dev, handle)] = buf
+
+
+def release_workspace(stream=None) -> None:
+    """Free the library-owned workspace of ``stream`` on the current device."""
+    _check(_L.o2m_release_workspace(_stream(stream)), "o2m_release_workspace")
 
 
 def get_status(stream=None) -> int:

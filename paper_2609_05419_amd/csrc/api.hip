@@ -9,6 +9,7 @@
 //   K4  2M post, CRT, symmetric lift, descale          (steps 4-7, eq. 2m-post)
 // and returns without synchronizing.
 #include <atomic>
+#include <map>
 #include <math.h>
 #include <mutex>
 #include <stdio.h>
@@ -25,16 +26,23 @@ constexpr int kMaxDevices = 64;
 constexpr int kPhaseCount = 4;
 constexpr int kMaxTimedCalls = 1024;
 
-struct DeviceState {
-    void *ws = nullptr;      // library-owned workspace
+// Scratch memory of the calls on one stream of one device.  Calls on the same
+// stream run one after another, so they can share it; calls on different
+// streams never do.
+struct StreamState {
+    void *ws = nullptr;       // library-owned workspace
     size_t ws_bytes = 0;
-    void *user_ws = nullptr; // caller-owned workspace (if set)
+    void *user_ws = nullptr;  // caller-owned workspace (if set)
     size_t user_bytes = 0;
-    int *status = nullptr;   // device status word
 };
 
 std::mutex g_mu;
-DeviceState g_dev[kMaxDevices];
+std::map<std::pair<int, hipStream_t>, StreamState> g_streams;
+
+// The device status word: a static device array (one per GPU), whose address
+// on each device is looked up once with that device current.
+__device__ __align__(256) int status_word[64];
+int *g_status[kMaxDevices];
 
 // phase timing (its own lock: every call takes a slot of events)
 std::mutex g_tmu;
@@ -132,27 +140,47 @@ o2m_status hip_fail(hipError_t e) {
         if (e_ != hipSuccess) return hip_fail(e_);           \
     } while (0)
 
-// Returns a device buffer of at least `bytes` on the current device.
-o2m_status workspace(size_t bytes, void **out, int **status) {
-    int dev = 0;
-    O2M_TRY(hipGetDevice(&dev));
-    if (dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
-    std::lock_guard<std::mutex> lock(g_mu);
-    DeviceState &d = g_dev[dev];
-    if (!d.status) {
-        O2M_TRY(hipMalloc((void **)&d.status, 256));
-        O2M_TRY(launch_zero(d.status, 256, nullptr));
-        O2M_TRY(hipDeviceSynchronize());
+// The status word of the current device (looked up on first use, under g_mu).
+o2m_status status_of(int dev, int **out) {
+    if (!g_status[dev]) {
+        void *p = nullptr;
+        O2M_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(status_word)));
+        g_status[dev] = (int *)p;
     }
-    *status = d.status;
+    *out = g_status[dev];
+    return O2M_OK;
+}
+
+o2m_status current_device(int *dev) {
+    O2M_TRY(hipGetDevice(dev));
+    return *dev >= 0 && *dev < kMaxDevices ? O2M_OK : O2M_ERR_HIP;
+}
+
+// Returns a device buffer of at least `bytes` for calls on stream st of the
+// current device: the caller's buffer bound to that stream, else the
+// library's buffer of that stream (allocated, or grown once the calls already
+// enqueued on st have finished).
+o2m_status workspace(hipStream_t st, size_t bytes, void **out, int **status) {
+    int dev = 0;
+    o2m_status s = current_device(&dev);
+    if (s != O2M_OK) return s;
+    std::lock_guard<std::mutex> lock(g_mu);
+    s = status_of(dev, status);
+    if (s != O2M_OK) return s;
+    StreamState &d = g_streams[std::make_pair(dev, st)];
     if (d.user_ws) {
         if (d.user_bytes < bytes) return O2M_ERR_WORKSPACE;
         *out = d.user_ws;
         return O2M_OK;
     }
     if (d.ws_bytes < bytes) {
-        // in-flight calls on any stream may still use the old buffer
-        O2M_TRY(hipDeviceSynchronize());
+        // a stream under graph capture can neither wait nor allocate: its
+        // workspace must be sized before the capture
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        O2M_TRY(hipStreamIsCapturing(st, &cs));
+        if (cs != hipStreamCaptureStatusNone) return O2M_ERR_WORKSPACE;
+        // earlier calls on this stream may still use the old buffer
+        O2M_TRY(hipStreamSynchronize(st));
         if (d.ws) O2M_TRY(hipFree(d.ws));
         d.ws = nullptr;
         d.ws_bytes = 0;
@@ -242,7 +270,7 @@ o2m_status run(const Call &c) {
     void *ws = nullptr;
     int *status = nullptr;
     const size_t need = carve(g, c.N, nullptr, nullptr);
-    s = workspace(need, &ws, &status);
+    s = workspace(c.st, need, &ws, &status);
     if (s != O2M_OK) return s;
     Buffers b;
     carve(g, c.N, ws, &b);
@@ -260,7 +288,7 @@ o2m_status run(const Call &c) {
     if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
     if (!sym) O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
     if (c.op != kOpG)
-        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, c.st));
+        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, status, c.st));
     if (cs) {
         O2M_TRY(launch_ssq(0, et, c.m, c.k, c.A, c.lda, b.E, b.ssq_a, c.st));
         if (two) O2M_TRY(launch_ssq(0, et, c.m, c.k, c.B, c.ldb, b.E, b.ssq_a, c.st));
@@ -574,25 +602,43 @@ size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli) {
     return carve(g, n_moduli, nullptr, nullptr);
 }
 
-o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes) {
+o2m_status o2m_set_workspace(void *dev_ptr, size_t bytes, void *stream) {
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
+    if (current_device(&dev) != O2M_OK) return O2M_ERR_HIP;
     std::lock_guard<std::mutex> lock(g_mu);
-    g_dev[dev].user_ws = dev_ptr;
-    g_dev[dev].user_bytes = dev_ptr ? bytes : 0;
+    StreamState &d = g_streams[std::make_pair(dev, (hipStream_t)stream)];
+    d.user_ws = dev_ptr;
+    d.user_bytes = dev_ptr ? bytes : 0;
+    return O2M_OK;
+}
+
+o2m_status o2m_release_workspace(void *stream) {
+    int dev = 0;
+    if (current_device(&dev) != O2M_OK) return O2M_ERR_HIP;
+    hipStream_t st = (hipStream_t)stream;
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_streams.find(std::make_pair(dev, st));
+    if (it == g_streams.end() || !it->second.ws) return O2M_OK;
+    if (hipStreamSynchronize(st) != hipSuccess) return O2M_ERR_HIP;
+    if (hipFree(it->second.ws) != hipSuccess) return O2M_ERR_HIP;
+    it->second.ws = nullptr;
+    it->second.ws_bytes = 0;
     return O2M_OK;
 }
 
 o2m_status o2m_get_status(void *stream, int *device_status) {
     if (!device_status) return -2;
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return O2M_ERR_HIP;
+    if (current_device(&dev) != O2M_OK) return O2M_ERR_HIP;
     hipStream_t st = (hipStream_t)stream;
     if (hipStreamSynchronize(st) != hipSuccess) return O2M_ERR_HIP;
-    int *p = g_dev[dev].status;
-    if (!p) { *device_status = 0; return O2M_OK; }
+    int *p = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        if (status_of(dev, &p) != O2M_OK) return O2M_ERR_HIP;
+    }
     if (hipMemcpy(device_status, p, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess) return O2M_ERR_HIP;
-    if (launch_zero(p, 256, st) != hipSuccess) return O2M_ERR_HIP;
+    if (launch_zero(p, sizeof(int), st) != hipSuccess) return O2M_ERR_HIP;
     if (hipStreamSynchronize(st) != hipSuccess) return O2M_ERR_HIP;
     return O2M_OK;
 }
@@ -626,7 +672,7 @@ const char *o2m_status_string(o2m_status s) {
     case O2M_OK: return "success";
     case O2M_ERR_NMODULI: return "n_moduli out of range (1..32 for GEMM, 1..22 for HERK/SYRK/rank-2k, 1..8 gauss)";
     case O2M_ERR_KLIMIT: return "k exceeds 149130 (131071 with more than 22 moduli): int32 accumulation bound";
-    case O2M_ERR_WORKSPACE: return "caller workspace too small";
+    case O2M_ERR_WORKSPACE: return "workspace too small (a caller buffer, or a stream under graph capture whose workspace was not sized before the capture)";
     case O2M_ERR_HIP: return "HIP runtime error";
     case O2M_ERR_NOMEM: return "workspace allocation failed";
     case O2M_ERR_SIZE: return "problem too large for the tile grid";

@@ -185,18 +185,27 @@ __global__ void cs_exponents_kernel(int ca, const unsigned long long *Ua, int32_
 }
 
 // Entries [0, ca) of (amax_a, Ea), then [0, cb) of (amax_b, Eb), in one launch.
+// A row or column holding Inf or NaN gets E = INT32_MIN and sets the device
+// status bit kStatusNonfinite (one atomic per wave that saw one).
 __global__ void exponents_kernel(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
-                                 const unsigned long long *amax_b, int32_t *Eb) {
+                                 const unsigned long long *amax_b, int32_t *Eb, int *status) {
     int i = blockIdx.x * 256 + threadIdx.x;
     const unsigned long long *amax = amax_a;
     int32_t *E = Ea;
-    if (i >= ca) { i -= ca; amax = amax_b; E = Eb; if (i >= cb) return; }
-    const unsigned long long b = amax[i];
-    int e;
-    if (b >= 0x7FF0000000000000ull) e = INT32_MIN;      // Inf or NaN in the row
-    else if (b == 0) e = 0;                                // zero row: E = 0
-    else frexp(__longlong_as_double((long long)b), &e);    // max < 2^e
-    E[i] = e;
+    bool valid = true;
+    if (i >= ca) { i -= ca; amax = amax_b; E = Eb; valid = i < cb; }
+    bool bad = false;
+    if (valid) {
+        const unsigned long long b = amax[i];
+        int e;
+        bad = b >= 0x7FF0000000000000ull;
+        if (bad) e = INT32_MIN;                                // Inf or NaN in the row
+        else if (b == 0) e = 0;                                // zero row: E = 0
+        else frexp(__longlong_as_double((long long)b), &e);    // max < 2^e
+        E[i] = e;
+    }
+    const unsigned long long seen = __ballot(bad);
+    if (seen != 0 && (int)(threadIdx.x & 63) == __ffsll((long long)seen) - 1) atomicOr(status, kStatusNonfinite);
 }
 
 __global__ void zero_kernel(uint4 *p, size_t n16, unsigned char *tail, int ntail) {
@@ -251,10 +260,10 @@ hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X,
 }
 
 hipError_t launch_exponents(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
-                            const unsigned long long *amax_b, int32_t *Eb, hipStream_t st) {
+                            const unsigned long long *amax_b, int32_t *Eb, int *status, hipStream_t st) {
     const int count = ca + cb;
     if (count <= 0) return hipSuccess;
-    exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(ca, amax_a, Ea, cb, amax_b, Eb);
+    exponents_kernel<<<(count + 255) / 256, 256, 0, st>>>(ca, amax_a, Ea, cb, amax_b, Eb, status);
     return hipGetLastError();
 }
 

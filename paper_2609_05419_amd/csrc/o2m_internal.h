@@ -14,7 +14,8 @@ constexpr int kMaxProducts = 2 * kMax2M + 3 * (kMaxModuli - kMax2M);  // int8 GE
 constexpr int kMaxLimbs = 6;
 constexpr int kMaxDigits = 5;     // base-2^26 digits of a quantized value (K2)
 constexpr int kLimbBits = 40;  // CRT limb base 2^40: limb sums stay below 2^53
-constexpr int kStatusOverflow = 1;  // device status bit: gauss-mode bound violated
+constexpr int kStatusOverflow = 1;   // device status bit: gauss-mode bound violated
+constexpr int kStatusNonfinite = 2;  // device status bit: a row / column held Inf or NaN
 
 // ---------------------------------------------------------------------------
 // Operand plane layout (the int8 residue planes A+-, B+- of eq. 2m-pre)
@@ -124,10 +125,11 @@ enum ElemType { kF64 = 0, kF32 = 1, kI32 = 2, kR64 = 3 /* real fp64 */ };
 // matrix, into amax bits (uint64, atomicMax of |x| bit patterns).
 hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X, int ld,
                        unsigned long long *amax, hipStream_t st);
-// K1 finish: amax bits -> exponents (INT32_MIN when non-finite), for ca rows
-// of A and cb columns of B in one launch.
+// K1 finish: amax bits -> exponents (INT32_MIN when non-finite, which also
+// ORs kStatusNonfinite into *status), for ca rows of A and cb columns of B in
+// one launch.
 hipError_t launch_exponents(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
-                            const unsigned long long *amax_b, int32_t *Eb, hipStream_t st);
+                            const unsigned long long *amax_b, int32_t *Eb, int *status, hipStream_t st);
 // K1, Cauchy-Schwarz rule: U_r += sum over the parts v of row (mode 0) or
 // column (mode 1) r of ceil(|v| 2^(20 - E_r))^2 (exact uint64 atomics; rows
 // with E_r = INT32_MIN are skipped), then E_r += d - 20 with d the smallest

@@ -32,7 +32,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "gauss_gemm_2m", "zgemm_2m_residues",
               "o2m_moduli", "o2m_budget", "o2m_workspace_bytes", "o2m_set_workspace",
-              "o2m_get_status", "o2m_phase_timing", "o2m_phase_times", "o2m_status_string"):
+              "o2m_release_workspace", "o2m_get_status", "o2m_phase_timing", "o2m_phase_times", "o2m_status_string"):
         assert f in names
 
 

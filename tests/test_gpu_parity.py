@@ -166,6 +166,7 @@ def test_zgemm_with_caller_workspace(o2m):
     need = o2m.workspace_bytes("z", 90, 60, 70, 16)
     ws = torch.empty(need, dtype=torch.uint8, device=DEV)
     o2m.set_workspace(ws)
+    del ws                                  # the binding keeps the buffer alive
     try:
         got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
         with pytest.raises(o2m.O2MError):
@@ -589,6 +590,88 @@ def test_cgemm_and_zherk_strided(o2m):
     assert same_bits(got[low], ref[low])
 
 
+def test_zgemm_caller_workspace_is_per_stream(o2m):
+    a = W.complex_matrix(90, 70, 43)
+    b = W.complex_matrix(70, 60, 44)
+    need = o2m.workspace_bytes("z", 90, 60, 70, 16)
+    s = torch.cuda.Stream()
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    o2m.set_workspace(ws, stream=s)            # only calls on s use (and are limited by) it
+    try:
+        big = W.complex_matrix(300, 70, 2)
+        got_big = host(o2m.zgemm_2m(to_dev(big), to_dev(b), n_moduli=16))   # current stream: library memory
+        with torch.cuda.stream(s):
+            got = o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16)
+            with pytest.raises(o2m.O2MError):
+                o2m.zgemm_2m(to_dev(big), to_dev(b), n_moduli=16)
+        s.synchronize()
+        got = host(got)
+    finally:
+        o2m.set_workspace(None, stream=s)
+    assert same_bits(got, O.oq_zgemm(a, b, 16))
+    assert same_bits(got_big, O.oq_zgemm(big, b, 16))
+    with pytest.raises(ValueError):
+        o2m.set_workspace(torch.empty(need, dtype=torch.uint8))               # host memory
+    with pytest.raises(ValueError):
+        o2m.set_workspace(torch.empty((need, 2), dtype=torch.uint8, device=DEV)[:, 0])  # strided
+    o2m.release_workspace(s)
+
+
+def test_concurrent_calls_on_two_streams(o2m):
+    """Calls that overlap on two streams have workspaces of their own: two
+    different-shape ZGEMMs enqueued back to back on two streams, several
+    times over, are bit-identical to the oracle at sampled entries and to the
+    same calls run one after another."""
+    shapes = [(1536, 1280, 1088, 16, 811), (1024, 1792, 1600, 12, 823)]
+    ops = []
+    for m, n, k, N, seed in shapes:
+        a = W.complex_matrix(m, k, seed, dist="phi", phi=0.5)
+        b = W.complex_matrix(k, n, seed + 1, dist="phi", phi=0.5)
+        ops.append((a, b, to_dev(a), to_dev(b), N))
+    serial = [host(o2m.zgemm_2m(A, B, n_moduli=N)) for _, _, A, B, N in ops]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    outs = []
+    for rep in range(3):
+        for (a, b, A, B, N), s in zip(ops, streams):
+            with torch.cuda.stream(s):
+                outs.append((rep, o2m.zgemm_2m(A, B, n_moduli=N)))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    for t, (rep, C) in enumerate(outs):
+        a, b, _, _, N = ops[t % 2]
+        got = host(C)
+        assert same_bits(got, serial[t % 2]), (rep, t % 2)
+        ent = _sample(rng, a.shape[0], b.shape[1], 300)
+        ref = O.oq_zgemm(a, b, N, entries=ent)
+        assert same_bits(np.array([got[i, j] for i, j in ent]), ref)
+    for s in streams:
+        o2m.release_workspace(s)
+
+
+def test_nonfinite_status_bit(o2m):
+    a = W.complex_matrix(70, 50, 71)
+    b = W.complex_matrix(50, 40, 72)
+    o2m.get_status()                                      # start clean
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    assert np.isfinite(got).all() and o2m.get_status() == 0
+    a[13, 7] = complex(np.nan, 0.0)                       # a NaN row of A
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    assert np.isnan(got[13, :]).all()
+    assert o2m.get_status() == o2m.STATUS_NONFINITE
+    assert o2m.get_status() == 0                          # cleared by the read
+    b2 = b.copy()
+    b2[3, 39] = complex(0.0, -np.inf)                     # an Inf column of B (last column)
+    host(o2m.cgemm_2m(to_dev(a.astype(np.complex64)), to_dev(b2.astype(np.complex64)), n_moduli=8))
+    assert o2m.get_status() == o2m.STATUS_NONFINITE
+    h = W.complex_matrix(60, 30, 73)
+    h[59, 0] = np.inf                                     # the last row of a HERK operand
+    o2m.zherk_2m(to_dev(h), n_moduli=16)
+    assert o2m.get_status() == o2m.STATUS_NONFINITE
+    o2m.zherk_2m(to_dev(W.complex_matrix(60, 30, 74)), n_moduli=16, scaling="cs")
+    assert o2m.get_status() == 0
+
+
 def test_calls_on_a_side_stream(o2m):
     a = W.complex_matrix(120, 100, 421)
     b = W.complex_matrix(100, 80, 422)
@@ -609,10 +692,12 @@ def _graph_replays(o2m, m, n, k, N, seeds, entries=None):
     replays); each replay must equal the oracle for the inputs it saw."""
     A = o2m.colmajor(torch.zeros((m, k), dtype=torch.complex128, device=DEV))
     B = o2m.colmajor(torch.zeros((k, n), dtype=torch.complex128, device=DEV))
-    o2m.zgemm_2m(A, B, n_moduli=N)  # sizes the workspace outside the capture
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o2m.zgemm_2m(A, B, n_moduli=N)  # sizes the capture stream's workspace outside the capture
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
+    with torch.cuda.graph(g, stream=s):
         C = o2m.zgemm_2m(A, B, n_moduli=N)
     for seed in seeds:
         a = W.complex_matrix(m, k, seed, dist="phi", phi=2.0)
@@ -625,6 +710,26 @@ def _graph_replays(o2m, m, n, k, N, seeds, entries=None):
             assert same_bits(got, O.oq_zgemm(a, b, N)), seed
         else:
             assert same_bits(np.array([got[i, j] for i, j in entries]), O.oq_zgemm(a, b, N, entries=entries)), seed
+    del g
+    o2m.release_workspace(s)
+
+
+def test_capture_without_a_sized_workspace_is_refused(o2m):
+    """A capture on a stream whose workspace is too small fails with
+    O2M_ERR_WORKSPACE and leaves the capture intact (nothing allocated or
+    synchronized inside it)."""
+    A = o2m.colmajor(torch.zeros((64, 64), dtype=torch.complex128, device=DEV))
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        with pytest.raises(o2m.O2MError) as e:
+            o2m.zgemm_2m(A, A, n_moduli=16)
+        C = A * 2                                          # the capture still works
+    assert e.value.status == -22
+    g.replay()
+    torch.cuda.synchronize()
+    assert (C == 0).all()
 
 
 def test_zgemm_in_a_hip_graph(o2m):
