@@ -112,6 +112,8 @@ typedef int o2m_status;
 #define O2M_ERR_SIZE (-25)      /* a padded size or plane offset exceeds the range  */
 #define O2M_ERR_SCALING (-26)   /* unknown scaling rule, or the Cauchy-Schwarz rule
                                    has no valid shifts for this n_moduli and k      */
+#define O2M_ERR_SCRATCH (-27)   /* zgemm_2m_noalloc: the call needs more than
+                                   O2M_NOALLOC_SCRATCH_BYTES of scratch memory      */
 
 /* scaling rules for the _ex calls */
 #define O2M_SCALE_MAX 0         /* max rule (what the plain calls use)              */
@@ -131,6 +133,22 @@ typedef int o2m_status;
 /* C = A B, A m x k, B k x n, complex128 (Section 3.2, Algorithm 1). */
 o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
                     double *C, int ldc, int n_moduli, void *stream);
+
+/* zgemm_2m_ex for callers that cannot allocate device memory (code under HIP
+   graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+   same computation and result, with every scratch buffer in a static device
+   array of O2M_NOALLOC_SCRATCH_BYTES (256 MiB) per GPU that the library holds
+   from its first such call on that GPU until the process ends.  The call
+   allocates nothing (no hipMalloc, hipFree or allocating library routine),
+   enqueues kernels only and returns O2M_ERR_SCRATCH, before anything is
+   enqueued, when the call needs more (o2m_workspace_bytes('z', ...) >
+   O2M_NOALLOC_SCRATCH_BYTES; e.g. m = n = k = 1024 at N = 16 fits, 2048^3
+   does not).  The caller passes A, B and C.  All zgemm_2m_noalloc calls on
+   one GPU share its array: calls that overlap in time on one GPU (on
+   different streams, or from several threads) race and give wrong results. */
+#define O2M_NOALLOC_SCRATCH_BYTES (256u << 20)
+o2m_status zgemm_2m_noalloc(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                            double *C, int ldc, int n_moduli, int scaling, void *stream);
 
 /* C = A B in complex64: fp32 inputs are widened exactly, the same algorithm
    runs, and the result is rounded once to fp32 (Section 3.2; accuracy near fp32

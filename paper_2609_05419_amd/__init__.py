@@ -18,7 +18,7 @@ import os
 import torch
 
 __all__ = [
-    "zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
+    "zgemm_2m", "zgemm_2m_noalloc", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
     "zgemm_2m_residues", "moduli", "budget", "shifts", "workspace_bytes", "set_workspace",
     "release_workspace", "get_status", "STATUS_OVERFLOW", "STATUS_NONFINITE", "phase_timing", "phase_times", "colmajor", "O2MError", "LIB_PATH", "SCALING",
 ]
@@ -32,6 +32,7 @@ _I, _P, _D = ctypes.c_int, ctypes.c_void_p, ctypes.c_double
 _C = ctypes.c_char
 _L.zgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
 _L.cgemm_2m.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
+_L.zgemm_2m_noalloc.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.zherk_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _P]
 _L.dsyrk_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _P]
 _L.zher2k_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
@@ -57,7 +58,7 @@ _L.o2m_phase_timing.argtypes = [_I]
 _L.o2m_phase_times.argtypes = [_P, _I]
 _L.o2m_status_string.argtypes = [_I]
 _L.o2m_status_string.restype = ctypes.c_char_p
-for _f in ("zgemm_2m", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex",
+for _f in ("zgemm_2m", "zgemm_2m_noalloc", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex",
            "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex", "zher2k_2m_ex", "dsyr2k_2m_ex", "gauss_gemm_2m",
            "zgemm_2m_residues", "zgemm_2m_residues_ex", "o2m_moduli", "o2m_budget", "o2m_shifts",
            "o2m_set_workspace", "o2m_release_workspace", "o2m_get_status", "o2m_phase_timing",
@@ -131,6 +132,24 @@ def zgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Te
     _check(_L.zgemm_2m_ex(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
                           n_moduli, _rule(scaling), _stream(stream)), "zgemm_2m")
     return C
+
+
+NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def zgemm_2m_noalloc(A: torch.Tensor, B: torch.Tensor, out: torch.Tensor, n_moduli: int = 16, stream=None,
+                     scaling: str = "max") -> torch.Tensor:
+    """zgemm_2m into the caller's ``out`` through the entry point that
+    allocates no device memory (its scratch is a static array of
+    NOALLOC_SCRATCH_BYTES per GPU; calls that overlap on one GPU race)."""
+    _check_operands(A, B, torch.complex128)
+    m, k = A.shape
+    n = B.size(1)
+    if out.dtype != torch.complex128 or not out.is_cuda or tuple(out.shape) != (m, n):
+        raise ValueError(f"out must be a complex128 device tensor of shape {(m, n)}")
+    _check(_L.zgemm_2m_noalloc(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+                               n_moduli, _rule(scaling), _stream(stream)), "zgemm_2m_noalloc")
+    return out
 
 
 def cgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 8, out: torch.Tensor | None = None,

@@ -44,6 +44,16 @@ std::map<std::pair<int, hipStream_t>, StreamState> g_streams;
 __device__ __align__(256) int status_word[64];
 int *g_status[kMaxDevices];
 
+// Scratch memory of zgemm_2m_noalloc: a static device array, one per GPU
+// (each GPU the library runs on holds its copy until the process ends).  In
+// host code `scratch` only stands in for the symbol; its device address on
+// each GPU is looked up once, with that GPU current, and kept in
+// g_scratch[device].  Every zgemm_2m_noalloc call on a GPU uses that GPU's
+// array, so such calls that overlap in time on one GPU race.
+constexpr size_t kScratchBytes = (size_t)O2M_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+void *g_scratch[kMaxDevices];
+
 // phase timing (its own lock: every call takes a slot of events)
 std::mutex g_tmu;
 std::atomic<bool> g_timing{false};
@@ -156,6 +166,25 @@ o2m_status current_device(int *dev) {
     return *dev >= 0 && *dev < kMaxDevices ? O2M_OK : O2M_ERR_HIP;
 }
 
+// The static scratch array of the current device as the workspace of a call
+// that must not allocate (looked up on the device's first such call).
+o2m_status static_scratch(size_t bytes, void **out, int **status) {
+    if (bytes > kScratchBytes) return O2M_ERR_SCRATCH;
+    int dev = 0;
+    o2m_status s = current_device(&dev);
+    if (s != O2M_OK) return s;
+    std::lock_guard<std::mutex> lock(g_mu);
+    s = status_of(dev, status);
+    if (s != O2M_OK) return s;
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        O2M_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return O2M_OK;
+}
+
 // Returns a device buffer of at least `bytes` for calls on stream st of the
 // current device: the caller's buffer bound to that stream, else the
 // library's buffer of that stream (allocated, or grown once the calls already
@@ -226,6 +255,7 @@ struct Call {
     hipStream_t st;
     int8_t *res_out;
     int32_t *E_out, *F_out;
+    bool noalloc = false;     // workspace = the static scratch array
 };
 
 bool is_sym(Op op) { return op == kOpH || op == kOpS || op == kOpH2 || op == kOpS2; }
@@ -270,7 +300,7 @@ o2m_status run(const Call &c) {
     void *ws = nullptr;
     int *status = nullptr;
     const size_t need = carve(g, c.N, nullptr, nullptr);
-    s = workspace(c.st, need, &ws, &status);
+    s = c.noalloc ? static_scratch(need, &ws, &status) : workspace(c.st, need, &ws, &status);
     if (s != O2M_OK) return s;
     Buffers b;
     carve(g, c.N, ws, &b);
@@ -450,6 +480,16 @@ o2m_status zgemm_2m_ex(int m, int n, int k, const double *A, int lda, const doub
     if (s != O2M_OK || m == 0 || n == 0) return s;
     return run(Call{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
                     nullptr, nullptr});
+}
+
+o2m_status zgemm_2m_noalloc(int m, int n, int k, const double *A, int lda, const double *B, int ldb,
+                            double *C, int ldc, int n_moduli, int scaling, void *stream) {
+    o2m_status s = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI_HYBRID);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    Call c{kOpZ, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr, nullptr, nullptr};
+    c.noalloc = true;
+    return run(c);
 }
 
 o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
@@ -677,6 +717,7 @@ const char *o2m_status_string(o2m_status s) {
     case O2M_ERR_NOMEM: return "workspace allocation failed";
     case O2M_ERR_SIZE: return "problem too large for the tile grid";
     case O2M_ERR_SCALING: return "unknown scaling rule, or no Cauchy-Schwarz shifts for this n_moduli and k";
+    case O2M_ERR_SCRATCH: return "zgemm_2m_noalloc: the call needs more than the static scratch array (O2M_NOALLOC_SCRATCH_BYTES)";
     default: break;
     }
     if (s < 0 && s >= -12) return "invalid argument (BLAS position = -status)";
