@@ -58,6 +58,17 @@ def load_traffic(workload_key: str):
     return d.get("traffic_bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(a, b, n_moduli, rows, cols):
     """The oracle (exact output of Algorithm 1) on a rows x cols block of C."""
     import oracle
@@ -68,9 +79,10 @@ def cpu_baseline(a, b, n_moduli, rows, cols):
     oracle.oq_zgemm(a, b, n_moduli, entries=ent)
     dt = time.perf_counter() - t0
     k = a.shape[1]
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle.omp_threads()
     return {"value": 8.0 * len(ent) * k / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
+            "omp_threads": threads, "os_cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": f"exact Algorithm-1 output (C oracle, OpenMP) on a {rows}x{cols} block of C, "
                       f"k={k}, {dt:.2f} s"}
 
@@ -102,6 +114,33 @@ def hbm_probe(torch) -> dict:
     return out
 
 
+def hbm_probe_hip(torch) -> dict:
+    """HBM rates of the probe library's streaming kernels (16-byte accesses,
+    2 GiB per buffer, the better of 1 and 4 chunks per thread): read only,
+    write only, copy, 1 read : 2 writes (the residue step's mix at N = 16),
+    2 reads : 1 write (the CRT's mix at N = 16)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2609_05419_amd", "libo2m_probe.so")
+    L = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    L.o2m_probe_hbm.argtypes = [ctypes.c_int, P, P, P, P, ctypes.c_size_t, ctypes.c_int, P, ctypes.c_void_p]
+    L.o2m_probe_hbm.restype = ctypes.c_double
+    n = 2 << 30
+    bufs = [torch.empty(n, dtype=torch.uint8, device="cuda") for _ in range(4)]
+    for x in bufs:
+        x.fill_(7)
+    sink = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    p = [x.data_ptr() for x in bufs]
+    out = {}
+    for name, kind in (("read_GBs", 0), ("write_GBs", 1), ("copy_GBs", 2), ("r1w2_GBs", 3), ("r2w1_GBs", 4)):
+        out[name] = round(max(L.o2m_probe_hbm(kind, p[0], p[1], p[2], p[3], n, chunks, sink.data_ptr(), st)
+                              for chunks in (1, 4)), 1)
+    del bufs, sink
+    torch.cuda.empty_cache()
+    return out
+
+
 def mfma_ceiling(torch) -> dict:
     """The int8 MFMA rate the chip sustains on register operands (no memory
     traffic), from the probe library: the practical ceiling of the int8 GEMM
@@ -119,7 +158,36 @@ def mfma_ceiling(torch) -> dict:
     for name, variant in (("mfma16x16x64_random_TOPS", 0), ("mfma16x16x64_zero_TOPS", 1),
                           ("mfma32x32x32_random_TOPS", 2)):
         res[name] = round(L.o2m_probe_int8_mfma(variant, blocks, iters, out.data_ptr(), st), 1)
+    L.o2m_probe_int8_mfma_residues.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p]
+    L.o2m_probe_int8_mfma_residues.restype = ctypes.c_double
+    clk = ctypes.c_double()
+    res["mfma16x16x64_residues241_TOPS"] = round(
+        L.o2m_probe_int8_mfma_residues(241, blocks, iters, out.data_ptr(), ctypes.addressof(clk), st), 1)
+    res["residues241_clock_GHz"] = round(clk.value, 3)
     return res
+
+
+def mfma_residue_mix(torch, moduli) -> dict:
+    """The probe on the symmetric residues of each modulus the call uses, as
+    the int8 GEMM meets them (equal work per modulus): N / sum(1 / rate)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2609_05419_amd", "libo2m_probe.so")
+    L = ctypes.CDLL(path)
+    L.o2m_probe_int8_mfma_residues.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p]
+    L.o2m_probe_int8_mfma_residues.restype = ctypes.c_double
+    blocks, iters = 2048, 256
+    out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    inv, clocks = 0.0, []
+    for q in moduli:
+        clk = ctypes.c_double()
+        r = L.o2m_probe_int8_mfma_residues(min(q, 256), blocks, iters, out.data_ptr(), ctypes.addressof(clk), st)
+        inv += 1.0 / r
+        clocks.append(clk.value)
+    return {"mfma16x16x64_residue_mix_TOPS": round(len(moduli) / inv, 1),
+            "residue_mix_clock_GHz": round(sum(clocks) / len(clocks), 3)}
 
 
 def error_curve() -> int:
@@ -399,9 +467,20 @@ def main() -> int:
         if with_extras:
             hbm["practical"] = hbm_probe(torch)
             try:
+                probe = hbm_probe_hip(torch)
+                hbm["probe"] = probe
+                hbm["scale_frac_of_probe_read"] = round(hbm["scale_GBs"] / probe["read_GBs"], 4)
+                hbm["residues_frac_of_probe_r1w2"] = round(hbm["residues_GBs"] / probe["r1w2_GBs"], 4)
+                hbm["crt_frac_of_probe_r2w1"] = round(hbm["crt_GBs"] / probe["r2w1_GBs"], 4)
+            except (OSError, AttributeError) as e:
+                log(f"bench: HBM probe skipped: {e}")
+            try:
                 ceiling = mfma_ceiling(torch)
                 ceiling["gemm_frac_of_random_ceiling"] = round(achieved / ceiling["mfma16x16x64_random_TOPS"], 4)
-            except OSError as e:
+                ceiling.update(mfma_residue_mix(torch, o2m.moduli(N)[0]))
+                ceiling["gemm_frac_of_residue_mix_ceiling"] = round(
+                    achieved / ceiling["mfma16x16x64_residue_mix_TOPS"], 4)
+            except (OSError, AttributeError) as e:
                 log(f"bench: MFMA probe skipped: {e}")
 
         cpu = None

@@ -409,6 +409,7 @@ def lib():
         L.oracle_round_scaled.argtypes = [P, I, I]
         L.oracle_round_scaled.restype = ctypes.c_double
         L.oracle_dd_gemm.argtypes = [I, I, I, P, I, P, I, P, P, I, I, P, P]
+        L.oracle_omp_threads.restype = I
         _lib = L
     return _lib
 
@@ -594,6 +595,11 @@ def round_scaled(v: int, scale: int, fmt: str = "f64") -> float:
     u = v & ((1 << 256) - 1)
     w = np.array([(u >> (64 * t)) & ((1 << 64) - 1) for t in range(4)], dtype=np.uint64)
     return lib().oracle_round_scaled(w.ctypes.data, scale, int(fmt == "f32"))
+
+
+def omp_threads() -> int:
+    """OpenMP threads the C oracle's parallel loops use."""
+    return int(lib().oracle_omp_threads())
 
 
 def round_i128(v: int) -> float:

@@ -44,6 +44,7 @@
  * its whole row or column of C NaN.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -442,3 +443,7 @@ void oracle_dd_gemm(int m, int n, int k, const double *A, int lda, const double 
         Chi[o + 1] = ih; Clo[o + 1] = il;
     }
 }
+
+/* Threads an OpenMP parallel region of the oracle uses (for the baseline
+   report). */
+int oracle_omp_threads(void) { return omp_get_max_threads(); }

@@ -10,9 +10,10 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libo2m.so")
 SOURCES = ["api.hip", "k_scale.hip", "k_residue.hip", "k_gemm.hip", "k_crt.hip", "moduli.cpp"]
-# measurement probe (the practical int8 MFMA ceiling), a library of its own
+# measurement probes (the practical int8 MFMA ceiling, HBM streaming rates), a
+# library of their own
 PROBE_LIB = os.path.join(HERE, "libo2m_probe.so")
-PROBE_SOURCES = ["probe_mfma.hip"]
+PROBE_SOURCES = ["probe_mfma.hip", "probe_hbm.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

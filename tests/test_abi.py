@@ -178,7 +178,7 @@ def test_probe_library_exports_its_header():
         pytest.skip("libo2m_probe.so not built")
     text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "o2m_probe.h")).read(), flags=re.S)
     names = re.findall(r"^\s*(?:double|int|void)\s*(\w+)\s*\(", text, flags=re.M)
-    assert names == ["o2m_probe_int8_mfma"]
+    assert names == ["o2m_probe_int8_mfma", "o2m_probe_int8_mfma_residues", "o2m_probe_hbm"]
     L = ctypes.CDLL(path)
     for n in names:
         assert hasattr(L, n)
@@ -188,3 +188,18 @@ def test_probe_library_exports_its_header():
     assert L.o2m_probe_int8_mfma(3, 1, 1, ctypes.c_void_p(0x1000), None) < 0
     assert L.o2m_probe_int8_mfma(0, 0, 1, ctypes.c_void_p(0x1000), None) < 0
     assert L.o2m_probe_int8_mfma(0, 1, 1, None, None) < 0
+    L.o2m_probe_int8_mfma_residues.restype = ctypes.c_double
+    L.o2m_probe_int8_mfma_residues.argtypes = [ctypes.c_int] * 3 + [ctypes.c_void_p] * 3
+    assert L.o2m_probe_int8_mfma_residues(2, 1, 1, ctypes.c_void_p(0x1000), None, None) < 0     # modulus
+    assert L.o2m_probe_int8_mfma_residues(257, 1, 1, ctypes.c_void_p(0x1000), None, None) < 0
+    assert L.o2m_probe_int8_mfma_residues(241, 1, 1, None, None, None) < 0
+    L.o2m_probe_hbm.restype = ctypes.c_double
+    L.o2m_probe_hbm.argtypes = [ctypes.c_int] + [ctypes.c_void_p] * 4 + [ctypes.c_size_t, ctypes.c_int] + \
+        [ctypes.c_void_p] * 2
+    fake = ctypes.c_void_p(0x1000)
+    assert L.o2m_probe_hbm(5, fake, fake, fake, fake, 1 << 20, 1, fake, None) < 0       # kind
+    assert L.o2m_probe_hbm(0, fake, None, None, None, 1 << 20, 1, None, None) < 0       # read needs a sink
+    assert L.o2m_probe_hbm(3, fake, None, fake, None, 1 << 20, 1, None, None) < 0       # 1R:2W needs d
+    assert L.o2m_probe_hbm(4, fake, None, fake, None, 1 << 20, 1, None, None) < 0       # 2R:1W needs b
+    assert L.o2m_probe_hbm(2, fake, None, fake, None, 8, 1, None, None) < 0              # below 16 bytes
+    assert L.o2m_probe_hbm(2, fake, None, fake, None, 1 << 20, 3, None, None) < 0        # chunks
