@@ -18,6 +18,7 @@ namespace o2m {
 
 constexpr double kTwo40 = 1099511627776.0;
 constexpr double kTwo80 = 1208925819614629174706176.0;
+constexpr double kTwo120 = 1329227995784915872903807060280344576.0;
 
 O2M_HD inline int64_t bits_of_f64(double x) { return __builtin_bit_cast(int64_t, x); }
 O2M_HD inline double f64_of_bits(int64_t b) { return __builtin_bit_cast(double, b); }
@@ -190,20 +191,51 @@ O2M_HD inline UW<LimbWords<T>::value> words_of(const double (&c)[T]) {
     return v;
 }
 
+// Four lifted limbs (|c_t| < 2^53) as three terms whose sum rounds like c.
+// The limbs are first carry-normalized into balanced base-2^40 digits
+// d_0..d_3 (|d_t| <= 2^39 below the top one; every step exact in fp64).  If
+// d_3 = 0, c = d_2 2^80 + d_1 2^40 + d_0 exactly.  Otherwise |c| > 2^118, so
+// every double near c, and every midpoint between two, is a multiple of 2^65,
+// and so is its distance from d_3 2^120 + d_2 2^80; the two lowest digits
+// then enter as their sum y rounded to odd: RO(y) lies strictly between the
+// same two doubles of y's scale as y (or equals y), and those doubles are
+// 2^27 apart at most, so no multiple of 2^65 separates y from RO(y) (such a
+// multiple would be an even double of y's scale, and RO(y) is odd).  Any
+// rounding of the three terms to nearest or to odd thus equals that of c.
+O2M_HD inline void top3_of4(double (&c)[4], double &a, double &b, double &low) {
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+        const double h = rint(c[t] * (1.0 / kTwo40));
+        c[t] = fma(-h, kTwo40, c[t]);
+        c[t + 1] += h;
+    }
+    const bool top = c[3] != 0.0;
+    a = top ? c[3] * kTwo120 : c[2] * kTwo80;
+    b = top ? c[2] * kTwo80 : c[1] * kTwo40;
+    low = top ? sum_round_odd(c[1] * kTwo40, c[0]) : c[0];
+}
+
 // Steps 5-7 for one component with fp64 output: the lifted limbs, then
-// RN(c 2^sc), one rounding.  T <= 3 rounds c with the exact limb sum (T = 2)
-// or the three-term sum and scales by 2^sc, which is exact unless the result
-// is subnormal; such results (and those that underflow to zero) are rounded
-// again from the exact integer at the subnormal quantum.  T >= 4 rounds
-// through a multiword integer (192 bits for T = 4, 256 bits for T = 5, 6).
+// RN(c 2^sc), one rounding.  T <= 4 rounds c with the exact limb sum (T = 2)
+// or the three-term sum (T = 3; T = 4 through top3_of4) and scales by 2^sc,
+// which is exact unless the result is subnormal; such results (and those that
+// underflow to zero) are rounded again from the exact integer at the
+// subnormal quantum.  T >= 5 rounds through a 256-bit integer.
 template <int T>
 O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double c[T];
     lift_limbs<T>(S, mlimb, inv_m, c);
-    if constexpr (T <= 3) {
+    if constexpr (T <= 4) {
         double x;
-        if constexpr (T == 2) x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
-        else x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        if constexpr (T == 2) {
+            x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
+        } else if constexpr (T == 3) {
+            x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        } else {
+            double a, b, low;
+            top3_of4(c, a, b, low);
+            x = sum3_rn(a, b, low);
+        }
         const double r = ldexp(x, sc);
         if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
         return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
@@ -212,27 +244,44 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     }
 }
 
-// Steps 5-7 with fp32 output (CGEMM): RN32(c 2^sc), one rounding.  For T <= 3
+// Steps 5-7 with fp32 output (CGEMM): RN32(c 2^sc), one rounding.  For T <= 4
 // the limb sum is rounded to odd in fp64 and then to fp32: a value rounded to
 // odd with 53 >= 24 + 2 bits rounds to nearest exactly as the exact value
 // does, in the normal and subnormal fp32 ranges alike, as long as the scaling
 // by 2^sc is exact in fp64 (true unless the fp64 value is subnormal, which
-// takes the multiword path).  T >= 4 rounds the multiword integer to 24 bits
+// takes the multiword path).  T >= 5 rounds the multiword integer to 24 bits
 // directly.
 template <int T>
 O2M_HD inline float lift_round_f32(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double c[T];
     lift_limbs<T>(S, mlimb, inv_m, c);
-    if constexpr (T <= 3) {
+    if constexpr (T <= 4) {
         double x;
-        if constexpr (T == 2) x = sum_round_odd(c[1] * kTwo40, c[0]);
-        else x = sum3_ro(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        if constexpr (T == 2) {
+            x = sum_round_odd(c[1] * kTwo40, c[0]);
+        } else if constexpr (T == 3) {
+            x = sum3_ro(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        } else {
+            double a, b, low;
+            top3_of4(c, a, b, low);
+            x = sum3_ro(a, b, low);
+        }
         const double r = ldexp(x, sc);
         if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return (float)r;
         return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
     } else {
         return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
     }
+}
+
+// The lifted limbs rounded once (tests): the same steps as lift_round /
+// lift_round_f32 after lift_limbs.
+template <int T>
+O2M_HD inline double round_lifted(const double (&c_in)[T], int sc, bool f32) {
+    // S = c with q = 0: lift_limbs leaves the limbs as they are when M's
+    // limbs are zero and 1/M is zero
+    const double zero[T] = {};
+    return f32 ? (double)lift_round_f32<T>(c_in, zero, 0.0, sc) : lift_round<T>(c_in, zero, 0.0, sc);
 }
 
 // The exact lifted integer (Gaussian-integer mode: M < 2^63, two limbs).

@@ -36,6 +36,17 @@ double t_round_limbs(const int64_t *limbs, int T, int sc) {
     for (int t = 0; t < T; ++t) o2m::add_shifted<4>(v, limbs[t], 40 * t);
     return o2m::round_words<4>(v, sc);
 }
+// lifted limbs (|c_t| < 2^53) rounded once into fp64 / fp32 after 2^sc
+double t_round_lifted(const double *c, int T, int sc, int f32) {
+    double c2[2], c3[3], c4[4], c5[5], c6[6];
+    switch (T) {
+    case 2: for (int t = 0; t < 2; ++t) c2[t] = c[t]; return o2m::round_lifted<2>(c2, sc, f32 != 0);
+    case 3: for (int t = 0; t < 3; ++t) c3[t] = c[t]; return o2m::round_lifted<3>(c3, sc, f32 != 0);
+    case 4: for (int t = 0; t < 4; ++t) c4[t] = c[t]; return o2m::round_lifted<4>(c4, sc, f32 != 0);
+    case 5: for (int t = 0; t < 5; ++t) c5[t] = c[t]; return o2m::round_lifted<5>(c5, sc, f32 != 0);
+    default: for (int t = 0; t < 6; ++t) c6[t] = c[t]; return o2m::round_lifted<6>(c6, sc, f32 != 0);
+    }
+}
 double t_lift_round(const double *S, int T, const double *mlimb, double inv_m, int sc, int f32) {
     switch (T) {
     case 2: return lift<2>(S, mlimb, inv_m, sc, f32);

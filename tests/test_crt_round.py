@@ -36,6 +36,8 @@ def lib(tmp_path_factory):
     L.t_sum_ro.restype = D
     L.t_round_limbs_fmt.argtypes = [P, I, I, I]
     L.t_round_limbs_fmt.restype = D
+    L.t_round_lifted.argtypes = [P, I, I, I]
+    L.t_round_lifted.restype = D
     return L
 
 
@@ -137,6 +139,59 @@ def test_multiword_rounding_into_format(lib, T, bits, fmt):
             got = narrow(lib.t_round_limbs_fmt(arr.ctypes.data, T, sc, int(fmt == "f32")), fmt)
             want = narrow(O.round_scaled(c, sc, fmt), fmt)
             assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, sc, got, want)
+
+
+def wild_limbs(c: int, T: int, rng: random.Random):
+    """Limbs of c with |c_t| < 2^52 that are far from normalized: large limbs
+    of opposite signs that cancel."""
+    while True:
+        limbs = [rng.randint(-(1 << 51), 1 << 51) for _ in range(T - 1)]
+        top = (c - sum(l << (40 * t) for t, l in enumerate(limbs)))
+        if top % (1 << (40 * (T - 1))) == 0 and abs(top >> (40 * (T - 1))) < 1 << 52:
+            return limbs + [top >> (40 * (T - 1))]
+        # fix the lowest limbs so that the remainder divides: adjust limb 0..T-2 exactly
+        rest = c
+        out = []
+        for t in range(T - 1):
+            lo = rest % (1 << 40) + rng.choice((0, -(1 << 40))) + (rng.randint(-(1 << 11), 1 << 11) << 40)
+            out.append(lo)
+            rest = (rest - lo) >> 40
+        if abs(rest) < 1 << 52 and all(abs(x) < 1 << 52 for x in out):
+            return out + [rest]
+
+
+@pytest.mark.parametrize("fmt", ["f64", "f32"])
+def test_four_limb_rounding_via_three_terms(lib, fmt):
+    """Four lifted limbs rounded through carry normalization and three terms
+    (the top digit's case split at 2^120), against the oracle's rounding: values
+    on both sides of 2^118 .. 2^121 with cancelling top digits, ties of 24- and
+    53-bit significands (+-1 and exact), small values held by large cancelling
+    limbs, and subnormal results."""
+    rng = random.Random(44 + (fmt == "f32"))
+    emin, prec = (-1022, 53) if fmt == "f64" else (-126, 24)
+    vals = []
+    for _ in range(1500):
+        vals.append(rng.randint(-(1 << 152), 1 << 152))
+    for _ in range(1500):   # d_3 = +-1 with the digit below of the opposite sign
+        s = rng.choice((1, -1))
+        vals.append(s * ((1 << 120) - rng.randint(0, 1 << 119)) + rng.randint(-(1 << 80), 1 << 80))
+    for _ in range(3000):
+        p = rng.choice((24, 53))
+        sh = rng.randint(2, 150 - p)
+        base = (rng.randint(1 << (p - 1), (1 << p) - 1) << sh) + (1 << (sh - 1))
+        v = base + rng.choice((-1, 0, 1, rng.randint(-(1 << 40), 1 << 40)))
+        vals.append(v if rng.random() < 0.5 else -v)
+    for _ in range(500):
+        vals.append(rng.randint(-(1 << 60), 1 << 60))
+    for c in vals:
+        limbs = wild_limbs(c, 4, rng) if rng.random() < 0.5 else split_limbs(c, 4, rng)
+        arr = np.array(limbs, dtype=np.float64)
+        assert sum(int(x) << (40 * t) for t, x in enumerate(limbs)) == c
+        n = abs(c).bit_length()
+        for sc in (rng.randint(-40, 40), emin - prec + 1 - rng.randint(0, n + 1)):
+            got = lib.t_round_lifted(arr.ctypes.data, 4, sc, int(fmt == "f32"))
+            want = narrow(O.round_scaled(c, sc, fmt), fmt)
+            assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, limbs, sc)
 
 
 @pytest.mark.parametrize("T,bits", [(4, 150), (5, 190), (6, 245)])
