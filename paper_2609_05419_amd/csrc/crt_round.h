@@ -191,87 +191,114 @@ O2M_HD inline UW<LimbWords<T>::value> words_of(const double (&c)[T]) {
     return v;
 }
 
-// Four lifted limbs (|c_t| < 2^53) as three terms whose sum rounds like c.
-// The limbs are first carry-normalized into balanced base-2^40 digits
-// d_0..d_3 (|d_t| <= 2^39 below the top one; every step exact in fp64).  If
-// d_3 = 0, c = d_2 2^80 + d_1 2^40 + d_0 exactly.  Otherwise |c| > 2^118, so
-// every double near c, and every midpoint between two, is a multiple of 2^65,
-// and so is its distance from d_3 2^120 + d_2 2^80; the two lowest digits
-// then enter as their sum y rounded to odd: RO(y) lies strictly between the
-// same two doubles of y's scale as y (or equals y), and those doubles are
-// 2^27 apart at most, so no multiple of 2^65 separates y from RO(y) (such a
-// multiple would be an even double of y's scale, and RO(y) is odd).  Any
-// rounding of the three terms to nearest or to odd thus equals that of c.
-O2M_HD inline void top3_of4(double (&c)[4], double &a, double &b, double &low) {
+constexpr double kTwo160 = 1461501637330902918203684832716283019655932542976.0;
+constexpr double kTwo200 = 1606938044258990275541962092341162602522202993782792835301376.0;
+
+// Lifted limbs (|c_t| < 2^53, T = 4..6) as three terms a, b, low whose sum
+// rounds like c, to nearest and to odd.  The limbs are first carry-normalized
+// into balanced base-2^40 digits d_0..d_{T-1} (|d_t| <= 2^39 below the top
+// one; every step exact in fp64).  With j the index of the top nonzero digit,
+// a = d_j 2^(40 j), b = d_{j-1} 2^(40 (j-1)) and low = the sum y of the lower
+// digits rounded to odd (exact when j <= 2: low = d_0).  For j >= 3,
+// |c| > 2^(40 j - 2), so every double near c and every midpoint between two
+// is a multiple of 2^(40 j - 55), and so is its distance from a + b (a
+// multiple of 2^(40 j - 40)).  |y| < 2^(40 j - 40) makes the doubles of y's
+// scale at most 2^(40 j - 93) apart, so such a multiple is a double of y's
+// scale with an even last bit: RO(y), odd unless it equals y, lies on the
+// same side of it as y.  Any rounding of a + b + low to nearest or to odd
+// thus equals that of c.  RO(y) itself: the exact three-term sum rounded to
+// odd for three digits, and for four digits the same construction one level
+// down (their top digit weighs 2^120, where the margin is 2^38 again).
+O2M_HD inline double ro_digits3(double d0, double d1, double d2) { return sum3_ro(d2 * kTwo80, d1 * kTwo40, d0); }
+
+O2M_HD inline double ro_digits4(double d0, double d1, double d2, double d3) {
+    return d3 != 0.0 ? sum3_ro(d3 * kTwo120, d2 * kTwo80, sum_round_odd(d1 * kTwo40, d0)) : ro_digits3(d0, d1, d2);
+}
+
+template <int T>
+O2M_HD inline void top3_of(double (&c)[T], double &a, double &b, double &low) {
+    static_assert(T >= 4 && T <= 6, "three-term reduction for four to six limbs");
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int t = 0; t + 1 < T; ++t) {
         const double h = rint(c[t] * (1.0 / kTwo40));
         c[t] = fma(-h, kTwo40, c[t]);
         c[t + 1] += h;
     }
-    const bool top = c[3] != 0.0;
-    a = top ? c[3] * kTwo120 : c[2] * kTwo80;
-    b = top ? c[2] * kTwo80 : c[1] * kTwo40;
-    low = top ? sum_round_odd(c[1] * kTwo40, c[0]) : c[0];
+    if constexpr (T == 6) {
+        if (c[5] != 0.0) {
+            a = c[5] * kTwo200;
+            b = c[4] * kTwo160;
+            low = ro_digits4(c[0], c[1], c[2], c[3]);
+            return;
+        }
+    }
+    if constexpr (T >= 5) {
+        if (c[4] != 0.0) {
+            a = c[4] * kTwo160;
+            b = c[3] * kTwo120;
+            low = ro_digits3(c[0], c[1], c[2]);
+            return;
+        }
+    }
+    if (c[3] != 0.0) {
+        a = c[3] * kTwo120;
+        b = c[2] * kTwo80;
+        low = sum_round_odd(c[1] * kTwo40, c[0]);
+    } else {
+        a = c[2] * kTwo80;
+        b = c[1] * kTwo40;
+        low = c[0];
+    }
 }
 
 // Steps 5-7 for one component with fp64 output: the lifted limbs, then
-// RN(c 2^sc), one rounding.  T <= 4 rounds c with the exact limb sum (T = 2)
-// or the three-term sum (T = 3; T = 4 through top3_of4) and scales by 2^sc,
+// RN(c 2^sc), one rounding.  c is rounded with the exact limb sum (T = 2) or
+// the three-term sum (T = 3; T >= 4 through top3_of) and scaled by 2^sc,
 // which is exact unless the result is subnormal; such results (and those that
-// underflow to zero) are rounded again from the exact integer at the
-// subnormal quantum.  T >= 5 rounds through a 256-bit integer.
+// underflow to zero) are rounded again from the exact integer, held as 192 or
+// 256 bits, at the subnormal quantum.
 template <int T>
 O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double c[T];
     lift_limbs<T>(S, mlimb, inv_m, c);
-    if constexpr (T <= 4) {
-        double x;
-        if constexpr (T == 2) {
-            x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
-        } else if constexpr (T == 3) {
-            x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
-        } else {
-            double a, b, low;
-            top3_of4(c, a, b, low);
-            x = sum3_rn(a, b, low);
-        }
-        const double r = ldexp(x, sc);
-        if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
-        return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
+    double x;
+    if constexpr (T == 2) {
+        x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
+    } else if constexpr (T == 3) {
+        x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
     } else {
-        return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
+        double a, b, low;
+        top3_of<T>(c, a, b, low);
+        x = sum3_rn(a, b, low);
     }
+    const double r = ldexp(x, sc);
+    if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
+    return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
 }
 
-// Steps 5-7 with fp32 output (CGEMM): RN32(c 2^sc), one rounding.  For T <= 4
-// the limb sum is rounded to odd in fp64 and then to fp32: a value rounded to
-// odd with 53 >= 24 + 2 bits rounds to nearest exactly as the exact value
-// does, in the normal and subnormal fp32 ranges alike, as long as the scaling
-// by 2^sc is exact in fp64 (true unless the fp64 value is subnormal, which
-// takes the multiword path).  T >= 5 rounds the multiword integer to 24 bits
-// directly.
+// Steps 5-7 with fp32 output (CGEMM): RN32(c 2^sc), one rounding.  The limb
+// sum is rounded to odd in fp64 and then to fp32: a value rounded to odd with
+// 53 >= 24 + 2 bits rounds to nearest exactly as the exact value does, in the
+// normal and subnormal fp32 ranges alike, as long as the scaling by 2^sc is
+// exact in fp64 (true unless the fp64 value is subnormal, which rounds the
+// multiword integer to 24 bits directly).
 template <int T>
 O2M_HD inline float lift_round_f32(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double c[T];
     lift_limbs<T>(S, mlimb, inv_m, c);
-    if constexpr (T <= 4) {
-        double x;
-        if constexpr (T == 2) {
-            x = sum_round_odd(c[1] * kTwo40, c[0]);
-        } else if constexpr (T == 3) {
-            x = sum3_ro(c[2] * kTwo80, c[1] * kTwo40, c[0]);
-        } else {
-            double a, b, low;
-            top3_of4(c, a, b, low);
-            x = sum3_ro(a, b, low);
-        }
-        const double r = ldexp(x, sc);
-        if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return (float)r;
-        return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
+    double x;
+    if constexpr (T == 2) {
+        x = sum_round_odd(c[1] * kTwo40, c[0]);
+    } else if constexpr (T == 3) {
+        x = sum3_ro(c[2] * kTwo80, c[1] * kTwo40, c[0]);
     } else {
-        return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
+        double a, b, low;
+        top3_of<T>(c, a, b, low);
+        x = sum3_ro(a, b, low);
     }
+    const double r = ldexp(x, sc);
+    if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return (float)r;
+    return (float)round_words_fmt<LimbWords<T>::value, 24, -126>(words_of<T>(c), sc);
 }
 
 // The lifted limbs rounded once (tests): the same steps as lift_round /

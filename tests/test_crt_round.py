@@ -160,36 +160,39 @@ def wild_limbs(c: int, T: int, rng: random.Random):
             return out + [rest]
 
 
+@pytest.mark.parametrize("T", [4, 5, 6])
 @pytest.mark.parametrize("fmt", ["f64", "f32"])
-def test_four_limb_rounding_via_three_terms(lib, fmt):
-    """Four lifted limbs rounded through carry normalization and three terms
-    (the top digit's case split at 2^120), against the oracle's rounding: values
-    on both sides of 2^118 .. 2^121 with cancelling top digits, ties of 24- and
-    53-bit significands (+-1 and exact), small values held by large cancelling
-    limbs, and subnormal results."""
-    rng = random.Random(44 + (fmt == "f32"))
+def test_many_limb_rounding_via_three_terms(lib, T, fmt):
+    """Four to six lifted limbs rounded through carry normalization and three
+    terms (split on the top nonzero digit), against the oracle's rounding:
+    values of every length, values just above and below each digit boundary
+    2^(40 j) with a cancelling digit below, ties of 24- and 53-bit significands
+    (+-1, exact, and with far-away low bits), small values held by large
+    cancelling limbs, and subnormal results."""
+    rng = random.Random(44 + 10 * T + (fmt == "f32"))
     emin, prec = (-1022, 53) if fmt == "f64" else (-126, 24)
+    top = 40 * (T - 1) + 12
     vals = []
-    for _ in range(1500):
-        vals.append(rng.randint(-(1 << 152), 1 << 152))
-    for _ in range(1500):   # d_3 = +-1 with the digit below of the opposite sign
-        s = rng.choice((1, -1))
-        vals.append(s * ((1 << 120) - rng.randint(0, 1 << 119)) + rng.randint(-(1 << 80), 1 << 80))
-    for _ in range(3000):
+    for _ in range(1200):
+        vals.append(rng.randint(-(1 << rng.randint(1, top)), 1 << rng.randint(1, top)))
+    for jb in range(1, T):   # the top digit d_j = +-1 with the digit below of the opposite sign
+        for _ in range(300):
+            s_ = rng.choice((1, -1))
+            vals.append(s_ * ((1 << (40 * jb)) - rng.randint(0, 1 << (40 * jb - 1)))
+                        + rng.randint(-(1 << (40 * jb - 40)), 1 << (40 * jb - 40)))
+    for _ in range(2500):
         p = rng.choice((24, 53))
-        sh = rng.randint(2, 150 - p)
+        sh = rng.randint(2, top - p - 2)
         base = (rng.randint(1 << (p - 1), (1 << p) - 1) << sh) + (1 << (sh - 1))
         v = base + rng.choice((-1, 0, 1, rng.randint(-(1 << 40), 1 << 40)))
         vals.append(v if rng.random() < 0.5 else -v)
-    for _ in range(500):
-        vals.append(rng.randint(-(1 << 60), 1 << 60))
     for c in vals:
-        limbs = wild_limbs(c, 4, rng) if rng.random() < 0.5 else split_limbs(c, 4, rng)
+        limbs = wild_limbs(c, T, rng) if rng.random() < 0.5 else split_limbs(c, T, rng)
         arr = np.array(limbs, dtype=np.float64)
         assert sum(int(x) << (40 * t) for t, x in enumerate(limbs)) == c
         n = abs(c).bit_length()
         for sc in (rng.randint(-40, 40), emin - prec + 1 - rng.randint(0, n + 1)):
-            got = lib.t_round_lifted(arr.ctypes.data, 4, sc, int(fmt == "f32"))
+            got = lib.t_round_lifted(arr.ctypes.data, T, sc, int(fmt == "f32"))
             want = narrow(O.round_scaled(c, sc, fmt), fmt)
             assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, limbs, sc)
 
