@@ -30,55 +30,46 @@ __device__ inline unsigned long long bits_of(double x) {
 
 __device__ inline unsigned long long umax(unsigned long long a, unsigned long long b) { return a > b ? a : b; }
 
-// Bit pattern of max(|Re|, |Im|) of one entry; a NaN in either part wins
-// (fmax would drop it).
-template <ElemType ET> struct Elem;
-template <> struct Elem<kF64> {
-    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
-        const double2 v = reinterpret_cast<const double2 *>(X)[idx];
-        return umax(bits_of(v.x), bits_of(v.y));
-    }
+// A NaN in either part of an entry wins the maximum (fmax would drop it):
+// bits() takes the larger bit pattern of |Re| and |Im|.
+// An entry as loaded, and what the two passes compute from it.  In column
+// mode a thread issues the loads of its kBatch rows of the chunk before using
+// any (a workgroup then reads 32 KB of one column at once).
+template <ElemType ET> struct Raw;
+template <> struct Raw<kF64> {
+    typedef double2 T;
+    static constexpr int n = 2;
+    static __device__ inline T load(const void *X, size_t idx) { return reinterpret_cast<const double2 *>(X)[idx]; }
+    static __device__ inline T zero() { return make_double2(0.0, 0.0); }
+    static __device__ inline unsigned long long bits(T v) { return umax(bits_of(v.x), bits_of(v.y)); }
+    static __device__ inline void parts(T v, double (&p)[2]) { p[0] = v.x; p[1] = v.y; }
 };
-template <> struct Elem<kF32> {
-    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
-        const float2 v = reinterpret_cast<const float2 *>(X)[idx];
-        return umax(bits_of((double)v.x), bits_of((double)v.y));
-    }
+template <> struct Raw<kF32> {
+    typedef float2 T;
+    static constexpr int n = 2;
+    static __device__ inline T load(const void *X, size_t idx) { return reinterpret_cast<const float2 *>(X)[idx]; }
+    static __device__ inline T zero() { return make_float2(0.0f, 0.0f); }
+    static __device__ inline unsigned long long bits(T v) { return umax(bits_of((double)v.x), bits_of((double)v.y)); }
+    static __device__ inline void parts(T v, double (&p)[2]) { p[0] = (double)v.x; p[1] = (double)v.y; }
 };
-template <> struct Elem<kI32> {
-    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
-        const int2 v = reinterpret_cast<const int2 *>(X)[idx];
-        return umax(bits_of((double)v.x), bits_of((double)v.y));
-    }
+template <> struct Raw<kI32> {
+    typedef int2 T;
+    static constexpr int n = 2;
+    static __device__ inline T load(const void *X, size_t idx) { return reinterpret_cast<const int2 *>(X)[idx]; }
+    static __device__ inline T zero() { return make_int2(0, 0); }
+    static __device__ inline unsigned long long bits(T v) { return umax(bits_of((double)v.x), bits_of((double)v.y)); }
+    static __device__ inline void parts(T v, double (&p)[2]) { p[0] = (double)v.x; p[1] = (double)v.y; }
 };
-template <> struct Elem<kR64> {
-    static __device__ inline unsigned long long bits(const void *X, size_t idx) {
-        return bits_of(reinterpret_cast<const double *>(X)[idx]);
-    }
+template <> struct Raw<kR64> {
+    typedef double T;
+    static constexpr int n = 1;
+    static __device__ inline T load(const void *X, size_t idx) { return reinterpret_cast<const double *>(X)[idx]; }
+    static __device__ inline T zero() { return 0.0; }
+    static __device__ inline unsigned long long bits(T v) { return bits_of(v); }
+    static __device__ inline void parts(T v, double (&p)[2]) { p[0] = v; p[1] = 0.0; }
 };
 
-// Parts of one entry for the Cauchy-Schwarz sum of squares.
-template <ElemType ET> struct Parts;
-template <> struct Parts<kF64> {
-    static constexpr int n = 2;
-    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
-        const double2 x = reinterpret_cast<const double2 *>(X)[idx];
-        v[0] = x.x; v[1] = x.y;
-    }
-};
-template <> struct Parts<kF32> {
-    static constexpr int n = 2;
-    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
-        const float2 x = reinterpret_cast<const float2 *>(X)[idx];
-        v[0] = (double)x.x; v[1] = (double)x.y;
-    }
-};
-template <> struct Parts<kR64> {
-    static constexpr int n = 1;
-    static __device__ inline void get(const void *X, size_t idx, double (&v)[2]) {
-        v[0] = reinterpret_cast<const double *>(X)[idx]; v[1] = 0.0;
-    }
-};
+constexpr int kBatch = 8;   // loads issued together per thread (column mode)
 
 // ceil(|v| 2^(20 - e))^2 for one part: |v| < 2^e, so the ceiling is at most
 // 2^20; a nonzero part whose scaled value underflows lies in (0, 1) and
@@ -102,10 +93,10 @@ __global__ __launch_bounds__(256) void amax_rows(int rows, int cols, int chunk, 
     const int c0 = blockIdx.y * chunk;
     const int c1 = min(cols, c0 + chunk);
     unsigned long long best = 0;
-    for (int c = c0; c < c1; ++c) {
-        unsigned long long b = Elem<ET>::bits(X, (size_t)r + (size_t)c * ld);
-        best = b > best ? b : best;
-    }
+    // one load in flight per thread: a workgroup's waves walk one column (4 KB
+    // contiguous) at a time; batching loads over columns opened more DRAM
+    // pages at once and measured slower at 8192^2 (faster only at 4096^2)
+    for (int c = c0; c < c1; ++c) best = umax(best, Raw<ET>::bits(Raw<ET>::load(X, (size_t)r + (size_t)c * ld)));
     if (best) atomicMax(amax + r, best);
 }
 
@@ -116,10 +107,15 @@ __global__ __launch_bounds__(256) void amax_cols(int rows, int cols, const void 
     const int r0 = blockIdx.y * kColChunk;
     const int r1 = min(rows, r0 + kColChunk);
     unsigned long long best = 0;
-    for (int r = r0 + threadIdx.x; r < r1; r += 256) {
-        unsigned long long b = Elem<ET>::bits(X, (size_t)r + (size_t)c * ld);
-        best = b > best ? b : best;
+    static_assert(kColChunk == 256 * kBatch, "one batch of loads per thread covers the chunk");
+    typename Raw<ET>::T v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+        const int r = r0 + threadIdx.x + 256 * u;
+        v[u] = r < r1 ? Raw<ET>::load(X, (size_t)r + (size_t)c * ld) : Raw<ET>::zero();
     }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) best = umax(best, Raw<ET>::bits(v[u]));
     // wave reduction, then one atomic per wave
     for (int off = 32; off > 0; off >>= 1) {
         unsigned long long o = __shfl_xor(best, off, 64);
@@ -140,12 +136,13 @@ __global__ __launch_bounds__(256) void ssq_rows(int rows, int cols, int chunk, c
     const int c0 = blockIdx.y * chunk;
     const int c1 = min(cols, c0 + chunk);
     unsigned long long acc = 0;
-    for (int c = c0; c < c1; ++c) {
+    auto add = [&](typename Raw<ET>::T x) {
         double v[2];
-        Parts<ET>::get(X, (size_t)r + (size_t)c * ld, v);
+        Raw<ET>::parts(x, v);
 #pragma unroll
-        for (int q = 0; q < Parts<ET>::n; ++q) acc += ssq_term(v[q], e);
-    }
+        for (int q = 0; q < Raw<ET>::n; ++q) acc += ssq_term(v[q], e);
+    };
+    for (int c = c0; c < c1; ++c) add(Raw<ET>::load(X, (size_t)r + (size_t)c * ld));
     if (acc) atomicAdd(U + r, acc);
 }
 
@@ -158,11 +155,18 @@ __global__ __launch_bounds__(256) void ssq_cols(int rows, int cols, const void *
     const int r0 = blockIdx.y * kColChunk;
     const int r1 = min(rows, r0 + kColChunk);
     unsigned long long acc = 0;
-    for (int r = r0 + threadIdx.x; r < r1; r += 256) {
-        double v[2];
-        Parts<ET>::get(X, (size_t)r + (size_t)c * ld, v);
+    typename Raw<ET>::T x[kBatch];
 #pragma unroll
-        for (int q = 0; q < Parts<ET>::n; ++q) acc += ssq_term(v[q], e);
+    for (int u = 0; u < kBatch; ++u) {
+        const int r = r0 + threadIdx.x + 256 * u;
+        x[u] = r < r1 ? Raw<ET>::load(X, (size_t)r + (size_t)c * ld) : Raw<ET>::zero();
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+        double v[2];
+        Raw<ET>::parts(x[u], v);
+#pragma unroll
+        for (int q = 0; q < Raw<ET>::n; ++q) acc += ssq_term(v[q], e);
     }
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
     if ((threadIdx.x & 63) == 0 && acc) atomicAdd(U + c, acc);
