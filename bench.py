@@ -503,7 +503,7 @@ def main() -> int:
         cpu = None
         if with_extras and not args.no_cpu_baseline and op == "zgemm":
             log("bench: CPU oracle baseline on a sample")
-            cpu = cpu_baseline(a_host, b_host, N, rows=min(m, 1536), cols=min(n, 2048), scaling=rule)
+            cpu = cpu_baseline(a_host, b_host, N, rows=min(m, 1024), cols=min(n, 1536), scaling=rule)
 
         return {
             "metric": metric,
