@@ -137,8 +137,9 @@ o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double 
 /* zgemm_2m_ex for callers that cannot allocate device memory (code under HIP
    graph capture, tight serving loops, harnesses that forbid hipMalloc): the
    same computation and result, with every scratch buffer in a static device
-   array of O2M_NOALLOC_SCRATCH_BYTES (256 MiB) per GPU that the library holds
-   from its first such call on that GPU until the process ends.  The call
+   array of O2M_NOALLOC_SCRATCH_BYTES (256 MiB) that is part of the library's
+   device code: every GPU the library's code is loaded on holds a copy until
+   the process ends, whether or not this call is used.  The call
    allocates nothing (no hipMalloc, hipFree or allocating library routine),
    enqueues kernels only and returns O2M_ERR_SCRATCH, before anything is
    enqueued, when the call needs more (o2m_workspace_bytes('z', ...) >
