@@ -45,7 +45,8 @@ __device__ __align__(256) int status_word[64];
 int *g_status[kMaxDevices];
 
 // Scratch memory of zgemm_2m_noalloc: a static device array, one per GPU
-// (each GPU the library runs on holds its copy until the process ends).  In
+// (every GPU the library's code is loaded on holds its copy until the
+// process ends, 256 MiB, whether or not the call is used).  In
 // host code `scratch` only stands in for the symbol; its device address on
 // each GPU is looked up once, with that GPU current, and kept in
 // g_scratch[device].  Every zgemm_2m_noalloc call on a GPU uses that GPU's
