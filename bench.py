@@ -386,8 +386,7 @@ def main() -> int:
         scale_bytes = 8.0 * 2 * n * k
         post_bytes = lambda N: (N + 4.0) * n * n
     if rule == "cs":
-        scale_bytes *= 2        # the maxima pass, then the sum-of-squares pass
-        desc += ", Cauchy-Schwarz scaling"
+        desc += ", Cauchy-Schwarz scaling"   # one pass as well: maxima and sums of squares together
     a_host, b_host = a, b
 
     def run_one(N: int, with_extras: bool) -> dict:

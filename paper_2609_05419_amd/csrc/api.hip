@@ -88,12 +88,14 @@ struct Geometry {
                               // (GEMM), 1 per modulus (HERK/SYRK/rank-2k)
     int planes;               // operand planes per side: products (GEMM), 2N (symmetric)
     bool shared_planes;       // symmetric ops: B planes are the A- planes
+    int kscan;                // columns of A (rows of B) that K1 walks: the call's k
+    int cs_ca, cs_cb;         // Cauchy-Schwarz chunks per row of A (one source) / column of B
 };
 
 // 2M moduli among the first N (the rest are the 3M extension of a hybrid set)
 int count_2m(int N) { return N < kMax2M ? N : kMax2M; }
 
-Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halves) {
+Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halves, int kscan) {
     Geometry g;
     g.rows_a = rows_a;
     g.rows_b = rows_b;
@@ -110,28 +112,44 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halve
     g.products = sym ? N : 2 * n2 + 3 * (N - n2);
     g.planes = sym ? 2 * N : g.products;
     g.shared_planes = sym;
+    g.kscan = kscan;
+    g.cs_ca = cs_chunks(0, rows_a, kscan);
+    g.cs_cb = sym ? 0 : cs_chunks(1, kscan, rows_b);
     return g;
 }
 
 struct Buffers {
-    unsigned long long *amax_a, *amax_b, *ssq_a, *ssq_b;
+    unsigned long long *amax_a, *amax_b;
     unsigned *queue;  // the int8 GEMM's slot counters
     int32_t *E, *F;
+    CsPartials csa, csb;  // Cauchy-Schwarz chunk records (rows of A, columns of B)
     int8_t *planes_a, *planes_b, *res;
 };
+
+CsPartials cs_partials(Carver &c, int chunks, int pitch) {
+    CsPartials p;
+    const size_t bytes = sizeof(unsigned long long) * (size_t)chunks * pitch;
+    p.mx = (unsigned long long *)c.take(bytes);
+    p.s2 = (unsigned long long *)c.take(bytes);
+    p.s1n = (unsigned long long *)c.take(bytes);
+    p.pitch = pitch;
+    p.chunks = chunks;
+    return p;
+}
 
 size_t carve(const Geometry &g, int N, void *base, Buffers *b) {
     Carver c(base);
     Buffers t;
-    // amax_a, amax_b, ssq_a, ssq_b and queue stay contiguous and in this
-    // order, ending where E begins: K1 clears them with one fill
+    // amax_a, amax_b and queue stay contiguous and in this order, ending
+    // where E begins: K1 clears them with one fill
     t.amax_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
     t.amax_b = g.shared_planes ? t.amax_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
-    t.ssq_a = (unsigned long long *)c.take(sizeof(unsigned long long) * g.a_pad);
-    t.ssq_b = g.shared_planes ? t.ssq_a : (unsigned long long *)c.take(sizeof(unsigned long long) * g.b_pad);
     t.queue = (unsigned *)c.take(sizeof(unsigned) * 8 * kQueueStride);
     t.E = (int32_t *)c.take(sizeof(int32_t) * g.a_pad);
     t.F = g.shared_planes ? t.E : (int32_t *)c.take(sizeof(int32_t) * g.b_pad);
+    // every record the combine step reads is written by the scan: no fill
+    t.csa = cs_partials(c, g.cs_ca * g.halves, g.a_pad);
+    t.csb = cs_partials(c, g.cs_cb, g.b_pad);
     t.planes_a = (int8_t *)c.take(g.plane_a * g.planes);
     t.planes_b = g.shared_planes ? t.planes_a : (int8_t *)c.take(g.plane_b * g.planes);
     t.res = (int8_t *)c.take(g.plane_c * g.products);
@@ -295,7 +313,7 @@ o2m_status run(const Call &c) {
     int pA = 0, pB = 0;
     o2m_status s = shifts(t, c.op, gemm_k(c.op, c.k), c.scaling, &pA, &pB);
     if (s != O2M_OK) return s;
-    const Geometry g = make_geometry(c.m, sym ? c.m : c.n, kc, c.N, sym, two ? 2 : 1);
+    const Geometry g = make_geometry(c.m, sym ? c.m : c.n, kc, c.N, sym, two ? 2 : 1, c.k);
     if ((long)g.a_pad * g.b_pad > (1L << 40) || (long)g.a_pad / kRowBlock * (g.b_pad / kRowBlock) * g.products > 0x7FFFFFFFL)
         return O2M_ERR_SIZE;
     void *ws = nullptr;
@@ -311,20 +329,39 @@ o2m_status run(const Call &c) {
     const int slot = phase_begin();
     phase_mark(slot, 0, c.st);
     // ---- K1: maxima and exponents (rank-2k: row i of A and of B share one) --
-    // maxima, sums of squares and the GEMM's slot counters start at zero: one
+    // the maxima (max rule) and the GEMM's slot counters start at zero: one
     // fill over the contiguous amax_a .. queue region of the workspace (carve
     // order)
     O2M_TRY(launch_zero(b.amax_a, (size_t)((char *)b.E - (char *)b.amax_a), c.st));
-    O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
-    if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
-    if (!sym) O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
-    if (c.op != kOpG)
-        O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, status, c.st));
-    if (cs) {
-        O2M_TRY(launch_ssq(0, et, c.m, c.k, c.A, c.lda, b.E, b.ssq_a, c.st));
-        if (two) O2M_TRY(launch_ssq(0, et, c.m, c.k, c.B, c.ldb, b.E, b.ssq_a, c.st));
-        if (!sym) O2M_TRY(launch_ssq(1, et, c.k, c.n, c.B, c.ldb, b.F, b.ssq_b, c.st));
-        O2M_TRY(launch_cs_exponents(c.m, b.ssq_a, b.E, sym ? 0 : c.n, b.ssq_b, b.F, c.st));
+    if (cs && c.op != kOpG) {
+        // one pass over each operand: chunk records, then the exponents they
+        // settle (the few entries they leave open are summed from the data)
+        O2M_TRY(launch_cs_scan(0, et, c.m, c.k, c.A, c.lda, b.csa, 0, c.st));
+        if (two) O2M_TRY(launch_cs_scan(0, et, c.m, c.k, c.B, c.ldb, b.csa, g.cs_ca, c.st));
+        if (!sym) O2M_TRY(launch_cs_scan(1, et, c.k, c.n, c.B, c.ldb, b.csb, 0, c.st));
+        CsCombineArgs cg;
+        memset(&cg, 0, sizeof cg);
+        cg.ca = c.m;
+        cg.cb = sym ? 0 : c.n;
+        cg.pa = b.csa;
+        cg.pb = b.csb;
+        cg.Ea = b.E;
+        cg.Eb = b.F;
+        cg.status = status;
+        cg.A = c.A;
+        cg.lda = c.lda;
+        cg.B2 = two ? c.B : nullptr;
+        cg.ldb2 = c.ldb;
+        cg.B = sym ? nullptr : c.B;
+        cg.ldb = c.ldb;
+        cg.k = c.k;
+        O2M_TRY(launch_cs_combine(et, cg, c.st));
+    } else {
+        O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
+        if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
+        if (!sym) O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
+        if (c.op != kOpG)
+            O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, status, c.st));
     }
     phase_mark(slot, 1, c.st);
 
@@ -639,7 +676,7 @@ size_t o2m_workspace_bytes(char op, int m, int n, int k, int n_moduli) {
     if (!op_of(op, &o) || n_moduli < 1 || m < 0 || n < 0 || k < 0) return 0;
     if (n_moduli > (is_sym(o) ? O2M_MAX_MODULI : o == kOpG ? 8 : O2M_MAX_MODULI_HYBRID)) return 0;
     const bool sym = is_sym(o);
-    const Geometry g = make_geometry(m, sym ? m : n, source_k(o, k), n_moduli, sym, is_rank2(o) ? 2 : 1);
+    const Geometry g = make_geometry(m, sym ? m : n, source_k(o, k), n_moduli, sym, is_rank2(o) ? 2 : 1, k);
     return carve(g, n_moduli, nullptr, nullptr);
 }
 

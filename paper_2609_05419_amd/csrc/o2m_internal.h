@@ -130,15 +130,36 @@ hipError_t launch_amax(int mode, ElemType et, int rows, int cols, const void *X,
 // one launch.
 hipError_t launch_exponents(int ca, const unsigned long long *amax_a, int32_t *Ea, int cb,
                             const unsigned long long *amax_b, int32_t *Eb, int *status, hipStream_t st);
-// K1, Cauchy-Schwarz rule: U_r += sum over the parts v of row (mode 0) or
-// column (mode 1) r of ceil(|v| 2^(20 - E_r))^2 (exact uint64 atomics; rows
-// with E_r = INT32_MIN are skipped), then E_r += d - 20 with d the smallest
-// d >= 0 such that 4^d >= U_r (U_r = 0 leaves E_r).
-hipError_t launch_ssq(int mode, ElemType et, int rows, int cols, const void *X, int ld, const int32_t *E,
-                      unsigned long long *U, hipStream_t st);
-hipError_t launch_cs_exponents(int ca, const unsigned long long *Ua, int32_t *Ea, int cb,
-                               const unsigned long long *Ub, int32_t *Eb, hipStream_t st);
-
+// K1, Cauchy-Schwarz rule, in one pass over each operand (cs_bounds.h).
+// Pass 1 (launch_cs_scan) writes one record per (row, chunk) of row (mode 0)
+// or column (mode 1) entries: the chunk's max |Re|,|Im| bit pattern, and the
+// sums S2 = sum y^2, S1 = sum y and the count n of nonzero parts, with
+// y = max(1, ceil(|v| 2^(20 - e))) against the chunk's own max exponent e.
+// Records live at [chunk][entry] with pitch `pitch`; a source's chunks start at
+// chunk_ofs (rank-2k rows: A's chunks, then B's).
+struct CsPartials {
+    unsigned long long *mx, *s2, *s1n;  // s1n = S1 | n << 44
+    int pitch;                          // entries per chunk row (padded rows)
+    int chunks;                         // chunks per entry, all sources
+};
+// Chunks per entry that one source of rows x cols gives in `mode`.
+int cs_chunks(int mode, int rows, int cols);
+hipError_t launch_cs_scan(int mode, ElemType et, int rows, int cols, const void *X, int ld, const CsPartials &p,
+                          int chunk_ofs, hipStream_t st);
+// Pass 2: E and the Cauchy-Schwarz exponent of every row of A (ca) and column
+// of B (cb) from the records (INT32_MIN and kStatusNonfinite for Inf/NaN, 0
+// for zero rows); an entry whose records leave the exponent open is summed
+// again from the operands (rows: A, and B2 for rank-2k updates; columns: B).
+struct CsCombineArgs {
+    int ca, cb;
+    CsPartials pa, pb;
+    int32_t *Ea, *Eb;
+    int *status;
+    const void *A, *B2, *B;
+    int lda, ldb2, ldb;
+    int k;                  // columns of A (rows of B)
+};
+hipError_t launch_cs_combine(ElemType et, const CsCombineArgs &g, hipStream_t st);
 // K2: quantize + residues + 2M pre into operand planes.
 //   mode 0: operand rows are rows of X (A, m x k), element (r, kk) at X[r + kk*ld]
 //   mode 1: operand rows are columns of X (B, k x n), element (r, kk) at X[kk + r*ld]

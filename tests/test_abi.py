@@ -67,9 +67,12 @@ def test_budget_matches_oracle():
 def test_workspace_bytes_grow_with_the_problem():
     import paper_2609_05419_amd as o2m
     z = o2m.workspace_bytes("z", 8192, 8192, 8192, 16)
-    # planes: 2N (m + n) k + 2N m n bytes, plus exponents
-    assert z >= 32 * (8192 * 8192 * 3)
-    assert z < 32 * (8192 * 8192 * 3) + (1 << 20)
+    # planes: 2N (m + n) k + 2N m n bytes, plus exponents and the
+    # Cauchy-Schwarz chunk records (24 bytes per row of A and 128 columns, per
+    # column of B and 2048 rows)
+    records = 24 * (8192 * (8192 // 128) + 8192 * (8192 // 2048))
+    assert z >= 32 * (8192 * 8192 * 3) + records
+    assert z < 32 * (8192 * 8192 * 3) + records + (1 << 20)
     h = o2m.workspace_bytes("h", 8192, 8192, 8192, 16)
     assert h < z
     s = o2m.workspace_bytes("s", 8192, 8192, 8192, 16)

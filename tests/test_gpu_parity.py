@@ -59,6 +59,7 @@ def test_gauss_config1_bit_exact(o2m):
     assert all((s * s + 1) % q == 0 for q, s in zip(ms, ss))
     dA = torch.from_numpy(A).to(DEV).transpose(0, 1)
     dB = torch.from_numpy(B).to(DEV).transpose(0, 1)
+    o2m.get_status()                                      # start clean
     C = o2m.gauss_gemm_2m(dA, dB, n_moduli=4)
     got = C.transpose(0, 1).cpu().numpy()
     assert o2m.get_status() == 0
@@ -669,6 +670,16 @@ def test_nonfinite_status_bit(o2m):
     o2m.zherk_2m(to_dev(h), n_moduli=16)
     assert o2m.get_status() == o2m.STATUS_NONFINITE
     o2m.zherk_2m(to_dev(W.complex_matrix(60, 30, 74)), n_moduli=16, scaling="cs")
+    assert o2m.get_status() == 0
+    # the Cauchy-Schwarz rule finds non-finite rows and columns in its one pass
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16, scaling="cs"))
+    assert np.isnan(got[13, :]).all() and o2m.get_status() == o2m.STATUS_NONFINITE
+    host(o2m.cgemm_2m(to_dev(a.astype(np.complex64) * 0 + 1), to_dev(b2.astype(np.complex64)), n_moduli=8,
+                      scaling="cs"))
+    assert o2m.get_status() == o2m.STATUS_NONFINITE
+    o2m.zherk_2m(to_dev(h), n_moduli=16, scaling="cs")
+    assert o2m.get_status() == o2m.STATUS_NONFINITE
+    host(o2m.zgemm_2m(to_dev(W.complex_matrix(70, 50, 75)), to_dev(b), n_moduli=16, scaling="cs"))
     assert o2m.get_status() == 0
 
 

@@ -86,9 +86,11 @@ def test_zgemm_cs_edge_cases(o2m):
     a[12, :] = 2.0 ** 7              # the norm is exactly a power of two
     a[13, ::3] = 1e300               # huge entries next to ordinary ones
     ref = O.oq_zgemm(a, b, 16, scaling="cs")
+    o2m.get_status()                                      # start clean
     got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16, scaling="cs"))
     assert same_bits(got, ref)
     assert np.isnan(got[10, :]).all() and np.isnan(got[:, 11]).all()
+    assert o2m.get_status() == o2m.STATUS_NONFINITE       # read and cleared
 
 
 def test_residue_hook_cs_exponents_and_residues(o2m):
@@ -280,3 +282,68 @@ def test_zher2k_4096_sampled(o2m):
     ent = _sample(np.random.default_rng(20), n, n, 32, lower=True)
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_zher2k(a, b, 16, entries=ent))
+
+
+# ------------------------------- one pass over each operand: re-summed entries
+# Rows (columns) built so that the per-chunk records of the one-pass scan do
+# not settle the exponent (tests/cs_inputs.py): the library sums them again
+# from the data, and everything must still equal the oracle bit for bit.
+
+
+def _straddle_operands(m, n, k, dtype=np.complex128):
+    from cs_inputs import straddle_vector
+    a = W.complex_matrix(m, k, 191, dist="phi", phi=0.5)
+    b = W.complex_matrix(k, n, 192, dist="phi", phi=0.5)
+    rows = {1: "low", 4: "high", m - 1: "low"}
+    cols = {0: "high", 3: "low", n - 1: "high"}
+    for i, kind in rows.items():
+        a[i, :] = straddle_vector(k, kind)
+    for j, kind in cols.items():
+        b[:, j] = straddle_vector(k, kind, exact=(0, 2048), binade=(2048, 2112), stride=2048)
+    return a.astype(dtype), b.astype(dtype), rows, cols
+
+
+def test_cs_resummed_entries_exponents_and_zgemm(o2m):
+    m, n, k, N = 40, 36, 4096, 16
+    a, b, rows, cols = _straddle_operands(m, n, k)
+    _, E, F = o2m.zgemm_2m_residues(to_dev(a), to_dev(b), n_moduli=N, scaling="cs")
+    E0, _, F0, _ = O.exponents(a, b, "cs")
+    E, F = E.cpu().numpy(), F.cpu().numpy()
+    for i in rows:
+        assert E0[i] == O.cs_exponent_exact(a[i, :])
+    for j in cols:
+        assert F0[j] == O.cs_exponent_exact(b[:, j])
+    ok_e = np.array_equal(E, E0) and np.array_equal(F, F0)
+    ref = O.oq_zgemm(a, b, N, scaling="cs")
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N, scaling="cs"))
+    ok = same_bits(got, ref)
+    report("cs re-summed zgemm", shape=(m, n, k), exponents=ok_e, bitexact=ok)
+    assert ok_e and ok
+
+
+def test_cs_resummed_entries_cgemm(o2m):
+    a, b, _, _ = _straddle_operands(24, 20, 4096, np.complex64)
+    ref = O.oq_cgemm(a, b, 8, scaling="cs")
+    assert same_bits(host(o2m.cgemm_2m(to_dev(a), to_dev(b), n_moduli=8, scaling="cs")), ref)
+
+
+def test_cs_resummed_rows_symmetric_calls(o2m):
+    from cs_inputs import straddle_vector
+    n, k, N = 30, 700, 16
+    a = W.complex_matrix(n, k, 193, dist="phi", phi=2.0)
+    b = W.complex_matrix(n, k, 194, dist="phi", phi=2.0)
+    for i, kind in ((0, "low"), (7, "high"), (n - 1, "high")):
+        a[i, :] = straddle_vector(k, kind)
+        b[i, :] = 0.0                 # rank-2k: the row of [A | B] is A's
+    ref = O.oq_zherk(a, N, scaling="cs")
+    got = host(o2m.zherk_2m(to_dev(a), n_moduli=N, scaling="cs"))
+    assert same_bits(got[LOW(n)], ref[LOW(n)])
+    ref = O.oq_zher2k(a, b, N, scaling="cs")
+    got = host(o2m.zher2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling="cs"))
+    assert same_bits(got[LOW(n)], ref[LOW(n)])
+    r = W.real_matrix(n, k, 195, dist="phi", phi=2.0)
+    for i, kind in ((2, "low"), (5, "high")):
+        r[i, :] = straddle_vector(k, kind, complex_=False)
+    ref = O.oq_dsyrk(r, N, scaling="cs")
+    got = host(o2m.dsyrk_2m(to_dev(r), n_moduli=N, scaling="cs"))
+    assert same_bits(got[LOW(n)], ref[LOW(n)])
