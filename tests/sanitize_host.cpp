@@ -6,8 +6,11 @@
 // oracle and Python integers.
 //
 //   stdin:  "r T sc f32 c_0 ... c_{T-1}" lines: the limbs of an integer,
-//           rounded once into fp64 (f32 = 0) or fp32 (f32 = 1) after 2^sc
-//   stdout: "r <bits of the double>" per input line, then the moduli tables
+//           rounded once into fp64 (f32 = 0) or fp32 (f32 = 1) after 2^sc;
+//           "b t S2 S1 n U" lines: one Cauchy-Schwarz chunk record one
+//           binade count t below the row maximum, and a sum U (cs_bounds.h)
+//   stdout: "r <bits of the double>" per r line, "b <lo> <hi> <d of U>" per b
+//           line, then the moduli tables
 //           ("m N log2M limbs P(k=1024) P(k=65536) cs_ok m_1 s_1 ... m_N s_N")
 //           and "sched <shapes checked>" after the tile-schedule coverage
 //           checks (which abort on a failure).
@@ -20,6 +23,7 @@
 #include <vector>
 
 #include "../paper_2609_05419_amd/csrc/crt_round.h"
+#include "../paper_2609_05419_amd/csrc/cs_bounds.h"
 #include "../paper_2609_05419_amd/csrc/o2m_internal.h"
 #include "../paper_2609_05419_amd/csrc/sym_schedule.h"
 #include "../paper_2609_05419_amd/csrc/tile_schedule.h"
@@ -75,6 +79,15 @@ long check_sym_schedule(int nb) {
 int main() {
     char line[4096];
     while (fgets(line, sizeof line, stdin)) {
+        if (line[0] == 'b') {
+            int t = 0;
+            uint64_t s2 = 0, s1 = 0, n = 0, U = 0, lo = 0, hi = 0;
+            if (sscanf(line + 1, "%d %" SCNu64 " %" SCNu64 " %" SCNu64 " %" SCNu64, &t, &s2, &s1, &n, &U) != 5)
+                fail("bad b line", t, 0);
+            o2m::cs_chunk_bounds(t, s2, s1, n, &lo, &hi);
+            printf("b %" PRIu64 " %" PRIu64 " %d\n", lo, hi, o2m::cs_d_of(U));
+            continue;
+        }
         if (line[0] != 'r') continue;
         int T = 0, sc = 0, f32 = 0, pos = 0;
         char *p = line + 1;

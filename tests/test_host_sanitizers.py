@@ -1,10 +1,13 @@
 """Host code under AddressSanitizer and UndefinedBehaviorSanitizer (no GPU).
 
 * The library's host code (moduli.cpp) and the header-only helpers shared by
-  kernels and host (crt_round.h, tile_schedule.h, sym_schedule.h) are built
-  with g++ into tests/sanitize_host.cpp's driver: its step-7 rounding of limb
-  integers is compared with the oracle's pinned rounding, its moduli tables
-  with the oracle's, and it checks the tile schedules' coverage itself.
+  kernels and host (crt_round.h, cs_bounds.h, tile_schedule.h,
+  sym_schedule.h) are built with g++ into tests/sanitize_host.cpp's driver:
+  its step-7 rounding of limb integers is compared with the oracle's pinned
+  rounding, its moduli tables with the oracle's, its Cauchy-Schwarz chunk
+  brackets with the regular host build's (tests/cs_bounds_host.cpp, pinned
+  against the rule's definition in tests/test_cs_bounds.py), and it checks the
+  tile schedules' coverage itself.
 * The C oracle (oracle/o2m_oracle.c) is built with gcc + OpenMP into
   tests/sanitize_oracle.c's driver and must give bit for bit the results of the
   regular oracle library on the same inputs.
@@ -77,9 +80,23 @@ def test_host_library_code_under_sanitizers(host_driver):
         sc = rng.choice((rng.randint(-80, 80), emin - prec + 1 - rng.randint(0, n + 1)))
         cases.append((c, sc, f32))
         lines.append(f"r {T} {sc} {int(f32)} " + " ".join(str(x) for x in _limbs(c, T, rng)))
+    bcases = []
+    for _ in range(3000):   # chunk records as the one-pass scan writes them (y <= 2^20, n <= 4096)
+        n = rng.randint(0, 4096)
+        ys = [rng.randint(1, 1 << 20) for _ in range(min(n, 8))]
+        s1 = sum(ys) * n // max(1, len(ys)) if n else 0
+        s2 = sum(y * y for y in ys) * n // max(1, len(ys)) if n else 0
+        s2 = max(min(s2, n << 40), s1)
+        bcases.append((rng.randint(0, 24), s2, s1, n, rng.randint(0, 1 << 58)))
+    lines += [f"b {t} {s2} {s1} {n} {U}" for t, s2, s1, n, U in bcases]
     r = subprocess.run([host_driver], input="\n".join(lines) + "\n", capture_output=True, text=True, env=ENV)
     assert r.returncode == 0, r.stderr[-4000:]
     out = r.stdout.splitlines()
+    got_b = [ln.split()[1:] for ln in out if ln.startswith("b ")]
+    assert len(got_b) == len(bcases)
+    ref = _cs_bounds_regular_build()
+    for (t, s2, s1, n, U), (lo, hi, d) in zip(bcases, got_b):
+        assert (int(lo), int(hi), int(d)) == ref(t, s2, s1, n, U)
     got = [ln for ln in out if ln.startswith("r ")]
     assert len(got) == len(cases)
     for (c, sc, f32), ln in zip(cases, got):
@@ -99,6 +116,26 @@ def test_host_library_code_under_sanitizers(host_driver):
         q = O.budget_cs(ms, 8192)
         assert bool(cs_ok) == (q is not None) and (q is None or (qa, qb) == tuple(q))
     assert any(ln.startswith("sched ") for ln in out)
+
+
+def _cs_bounds_regular_build():
+    """The chunk bracket and d of the regular (unsanitized) host build."""
+    import ctypes
+    import tempfile
+    out = os.path.join(tempfile.mkdtemp(), "libcs_bounds_host.so")
+    subprocess.run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", os.path.join(HERE, "cs_bounds_host.cpp"),
+                    "-o", out], check=True)
+    L = ctypes.CDLL(out)
+    U64 = ctypes.c_uint64
+    L.t_cs_d_of.argtypes = [U64]
+    L.t_cs_d_of.restype = ctypes.c_int
+    L.t_cs_chunk_bounds.argtypes = [ctypes.c_int, U64, U64, U64, ctypes.POINTER(U64), ctypes.POINTER(U64)]
+
+    def f(t, s2, s1, n, U):
+        lo, hi = U64(), U64()
+        L.t_cs_chunk_bounds(t, s2, s1, n, ctypes.byref(lo), ctypes.byref(hi))
+        return lo.value, hi.value, L.t_cs_d_of(U)
+    return f
 
 
 def test_oracle_under_sanitizers(tmp_path):
