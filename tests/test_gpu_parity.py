@@ -697,30 +697,34 @@ def test_calls_on_a_side_stream(o2m):
     assert same_bits(np.asfortranarray(C2.cpu().numpy()), O.oq_zgemm(a, b, 12))
 
 
-def _graph_replays(o2m, m, n, k, N, seeds, entries=None):
+def _graph_replays(o2m, m, n, k, N, seeds, entries=None, scaling="max", edit=None):
     """Capture one zgemm_2m call into a HIP graph and replay it on fresh
     inputs copied into the captured buffers (eager copies and a sync between
-    replays); each replay must equal the oracle for the inputs it saw."""
+    replays); each replay must equal the oracle for the inputs it saw.
+    ``edit(seed, a)`` may change A's rows before a replay."""
     A = o2m.colmajor(torch.zeros((m, k), dtype=torch.complex128, device=DEV))
     B = o2m.colmajor(torch.zeros((k, n), dtype=torch.complex128, device=DEV))
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
-        o2m.zgemm_2m(A, B, n_moduli=N)  # sizes the capture stream's workspace outside the capture
+        o2m.zgemm_2m(A, B, n_moduli=N, scaling=scaling)  # sizes the capture stream's workspace outside the capture
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
-        C = o2m.zgemm_2m(A, B, n_moduli=N)
+        C = o2m.zgemm_2m(A, B, n_moduli=N, scaling=scaling)
     for seed in seeds:
         a = W.complex_matrix(m, k, seed, dist="phi", phi=2.0)
         b = W.complex_matrix(k, n, seed + 1, dist="phi", phi=2.0)
+        if edit:
+            edit(seed, a)
         A.copy_(to_dev(a))
         B.copy_(to_dev(b))
         g.replay()
         got = host(C)
         if entries is None:
-            assert same_bits(got, O.oq_zgemm(a, b, N)), seed
+            assert same_bits(got, O.oq_zgemm(a, b, N, scaling=scaling)), seed
         else:
-            assert same_bits(np.array([got[i, j] for i, j in entries]), O.oq_zgemm(a, b, N, entries=entries)), seed
+            ref = O.oq_zgemm(a, b, N, entries=entries, scaling=scaling)
+            assert same_bits(np.array([got[i, j] for i, j in entries]), ref), seed
     del g
     o2m.release_workspace(s)
 
@@ -748,6 +752,20 @@ def test_zgemm_in_a_hip_graph(o2m):
     once the workspace is sized; three replays on three inputs, bit-exact."""
     print("[parity] graph replays 300x270x520 N=16", flush=True)
     _graph_replays(o2m, 300, 270, 520, 16, seeds=(9401, 9403, 9405))
+
+
+def test_zgemm_cs_in_a_hip_graph(o2m):
+    """The Cauchy-Schwarz rule's one-pass scaling is capturable too, including
+    the rows its chunk records leave open (summed again inside the graph): the
+    second replay holds two such rows, the third none."""
+    from cs_inputs import straddle_vector
+
+    def edit(seed, a):
+        if seed == 9423:
+            a[5, :] = straddle_vector(a.shape[1], "low")
+            a[200, :] = straddle_vector(a.shape[1], "high")
+    print("[parity] graph replays 300x270x520 N=16, Cauchy-Schwarz rule", flush=True)
+    _graph_replays(o2m, 300, 270, 520, 16, seeds=(9421, 9423, 9425), scaling="cs", edit=edit)
 
 
 @pytest.mark.slow
