@@ -18,7 +18,8 @@
 // likewise I for x_im.  The host picks D from the bound on |x| so that the top
 // digit stays below 2^36 (D = 2 up to 2^62, 3 up to 2^88; D = 4, 5 keep it
 // below 2^30 and hold the digits as int32), which keeps |R| < 2^43.01 and
-// A+- = R +- s I an exact integer below 2^51 (s <= 120).  q = rint(A / m)
+// A+- = R +- s I an exact integer below 2^51 (s <= 120).  Up to |x| <= 2^44
+// no split is needed (D = 1: R = x, and |A+-| <= 121 2^44 < 2^51).  q = rint(A / m)
 // comes out of one fma against 1.5 2^52 (the low word of the sum is q), and
 // A - q m, needed only modulo 2^8, is one 24-bit integer multiply-add on the
 // low words.
@@ -99,9 +100,9 @@ __device__ inline void store_words(int8_t *dst, const uint32_t (&w)[PT / 4]) {
 // MODE 0: rows of X (A, column-major m x k): entry (r, kk) at X[r + kk*ld]
 // MODE 1: columns of X (B, column-major k x n): entry (r, kk) at X[kk + r*ld]
 // MODE 2: SYRK, X real column-major n x k: (r, kk) = X[r + kk ld] + i X[r + (kk+kh) ld]
-// D: base-2^26 digits of the quantized values (2..5, from their bound)
+// D: base-2^26 digits of the quantized values (1..5, from their bound)
 template <int MODE, ElemType ET, int D, bool SCALED>
-__global__ __launch_bounds__(256) void residue_kernel(const void *X, int ld, const int32_t *E,
+__global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void *X, int ld, const int32_t *E,
                                                       int shift, int khalf, int kreal, int rows, int k,
                                                       int rows_pad, int kblocks, int plane_kblocks,
                                                       int kofs_p, int kofs_m, size_t plane_bytes,
@@ -245,6 +246,7 @@ hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const i
                                                         planes)
 #define O2M_RES_D(M, T)                                       \
     switch (digits) {                                         \
+    case 1: O2M_RES(M, T, 1, true); break;                    \
     case 2: O2M_RES(M, T, 2, true); break;                    \
     case 3: O2M_RES(M, T, 3, true); break;                    \
     case 4: O2M_RES(M, T, 4, true); break;                    \

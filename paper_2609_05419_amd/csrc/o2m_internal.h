@@ -181,11 +181,11 @@ struct PlaneGeom {
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
                            int digits, int khalf, const PlaneGeom &g, const ResidueParams &rp,
                            int8_t *planes, hipStream_t st);
-// Digits for quantized values below 2^bits: 2 up to 62 bits, 3 up to 88
-// (top digit < 2^36), 4 up to 108 and 5 up to 134 (top digit < 2^30, int32);
-// 0 if more are needed.
+// Digits for quantized values below 2^bits: 1 up to 44 bits (no split), 2 up
+// to 62, 3 up to 88 (top digit < 2^36), 4 up to 108 and 5 up to 134 (top digit
+// < 2^30, int32); 0 if more are needed.
 inline int residue_digits(int bits) {
-    return bits <= 62 ? 2 : bits <= 88 ? 3 : bits <= 108 ? 4 : bits <= 134 ? 5 : 0;
+    return bits <= 44 ? 1 : bits <= 62 ? 2 : bits <= 88 ? 3 : bits <= 108 ? 4 : bits <= 134 ? 5 : 0;
 }
 
 // K3: batched int8 GEMM  C_p = A_p B_p^T  (both operands K-major planes), then

@@ -817,3 +817,29 @@ def test_zgemm_k_at_the_int32_limit_sampled(o2m):
     ent = [(0, 0), (m - 1, n - 1)] + [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 30), rng.integers(0, n, 30))]
     got = np.array([C[i, j] for i, j in ent])
     assert same_bits(got, O.oq_zgemm(a, b, 16, entries=ent))
+
+
+# The residue kernel reduces quantized values below 2^44 without splitting them
+# into base-2^26 digits; above that they are split.  Shapes whose shifts sit on
+# either side of that bound (operands on different sides in one call), with
+# entries that quantize to exactly +-2^p.
+DIGIT_CASES = [("max", 13, 64), ("max", 13, 128), ("max", 13, 256), ("max", 14, 8192), ("cs", 11, 100),
+               ("cs", 12, 100)]
+
+
+@pytest.mark.parametrize("rule,N,k", DIGIT_CASES, ids=[f"{r}-N{n}-k{k}" for r, n, k in DIGIT_CASES])
+def test_residue_digit_boundaries(o2m, rule, N, k):
+    m, n = 40, 24
+    a = W.complex_matrix(m, k, 8800 + k, dist="phi", phi=2.0)
+    b = W.complex_matrix(k, n, 8900 + k, dist="phi", phi=2.0)
+    below = np.nextafter(1.0, 0.0)           # just below 2^0: quantizes to 2^p under the max rule
+    a[3, :] = 0.5
+    a[3, 0] = complex(below, -below)
+    b[:, 4] = -0.25
+    b[7, 4] = complex(-below / 2, below / 2)
+    pA, pB = O.shifts(rule, O.moduli_set(N), k)
+    ref = O.oq_zgemm(a, b, N, scaling=rule)
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+    ok = same_bits(got, ref)
+    report("digit boundary", rule=rule, N=N, k=k, pA=pA, pB=pB, bitexact=ok)
+    assert ok
