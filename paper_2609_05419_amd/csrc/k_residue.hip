@@ -101,7 +101,12 @@ __device__ inline void store_words(int8_t *dst, const uint32_t (&w)[PT / 4]) {
 // MODE 1: columns of X (B, column-major k x n): entry (r, kk) at X[kk + r*ld]
 // MODE 2: SYRK, X real column-major n x k: (r, kk) = X[r + kk ld] + i X[r + (kk+kh) ld]
 // D: base-2^26 digits of the quantized values (1..5, from their bound)
-template <int MODE, ElemType ET, int D, bool SCALED>
+// PAIRS (complex fp32, the host sets it when every pair is 16-byte aligned):
+// MODE 1 reads two consecutive entries of a column of B per 16-byte load;
+// MODE 0 reads rows 2i, 2i + 1 of a column of A per 16-byte load, the even
+// lane of a lane pair columns kk0..kk0+7 and the odd lane kk0+8..kk0+15, and
+// the pair then swaps halves so that each lane holds its own row's 16 entries
+template <int MODE, ElemType ET, int D, bool SCALED, bool PAIRS = false>
 __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void *X, int ld, const int32_t *E,
                                                       int shift, int khalf, int kreal, int rows, int k,
                                                       int rows_pad, int kblocks, int plane_kblocks,
@@ -136,29 +141,80 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
         if (e == INT32_MIN) live = false;    // non-finite row: output masked later
         else sh = shift - e;
     }
-#pragma unroll
-    for (int e = 0; e < PT; ++e) {
-        const int kk = kk0 + e;
-        double vr = 0.0, vi = 0.0;
-        if (live && kk < k) {
-            if (MODE == 0) {
-                const double2 v = Load<ET>::get(X, (size_t)r + (size_t)kk * ld);
-                vr = v.x; vi = v.y;
-            } else if (MODE == 1) {
-                const double2 v = Load<ET>::get(X, (size_t)kk + (size_t)r * ld);
-                vr = v.x; vi = v.y;
-            } else {
-                const double *Xr = reinterpret_cast<const double *>(X);
-                vr = Xr[(size_t)r + (size_t)kk * ld];
-                if (kk + khalf < kreal) vi = Xr[(size_t)r + (size_t)(kk + khalf) * ld];
-            }
-        }
+    auto put = [&](int e, double vr, double vi) {
+        if (!live) vr = vi = 0.0;
         if (SCALED) {
             vr = rint(ldexp(vr, sh));
             vi = rint(ldexp(vi, sh));
         }
         split_digits<D, PT>(vr, xr, e);
         split_digits<D, PT>(vi, xi, e);
+    };
+    if constexpr (PAIRS && MODE == 0) {
+        static_assert(ET == kF32 && PT == 16, "pairs of complex fp32 rows, one lane chunk per lane");
+        const bool odd = lane & 1;
+        const int re = r - (int)odd;                 // the pair's even row
+        const float2 *Xa = reinterpret_cast<const float2 *>(X);
+        float4 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int kk = kk0 + (odd ? 8 : 0) + j;
+            v[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (kk < k) {
+                if (re + 1 < rows) {
+                    v[j] = *reinterpret_cast<const float4 *>(Xa + (size_t)re + (size_t)kk * ld);
+                } else if (re < rows) {
+                    const float2 t = Xa[(size_t)re + (size_t)kk * ld];
+                    v[j].x = t.x;
+                    v[j].y = t.y;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            // the even lane passes on its odd row's half, the odd lane its even row's
+            const float rx = __shfl_xor(odd ? v[j].x : v[j].z, 1, 64);
+            const float ry = __shfl_xor(odd ? v[j].y : v[j].w, 1, 64);
+            put(j, odd ? rx : v[j].x, odd ? ry : v[j].y);
+            put(8 + j, odd ? v[j].z : rx, odd ? v[j].w : ry);
+        }
+    } else if constexpr (PAIRS) {
+        static_assert(MODE == 1 && ET == kF32, "pairs of complex fp32 entries along a column");
+        const float2 *Xc = reinterpret_cast<const float2 *>(X) + (size_t)r * ld;
+#pragma unroll
+        for (int e = 0; e < PT; e += 2) {
+            const int kk = kk0 + e;
+            float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (live && kk + 1 < k) {
+                v = *reinterpret_cast<const float4 *>(Xc + kk);
+            } else if (live && kk < k) {
+                const float2 t = Xc[kk];
+                v.x = t.x;
+                v.y = t.y;
+            }
+            put(e, (double)v.x, (double)v.y);
+            put(e + 1, (double)v.z, (double)v.w);
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < PT; ++e) {
+            const int kk = kk0 + e;
+            double vr = 0.0, vi = 0.0;
+            if (live && kk < k) {
+                if (MODE == 0) {
+                    const double2 v = Load<ET>::get(X, (size_t)r + (size_t)kk * ld);
+                    vr = v.x; vi = v.y;
+                } else if (MODE == 1) {
+                    const double2 v = Load<ET>::get(X, (size_t)kk + (size_t)r * ld);
+                    vr = v.x; vi = v.y;
+                } else {
+                    const double *Xr = reinterpret_cast<const double *>(X);
+                    vr = Xr[(size_t)r + (size_t)kk * ld];
+                    if (kk + khalf < kreal) vi = Xr[(size_t)r + (size_t)(kk + khalf) * ld];
+                }
+            }
+            put(e, vr, vi);
+        }
     }
 
     // ---- residues and 2M pre per modulus (step 4, eq. 2m-pre) -------------
@@ -239,27 +295,41 @@ hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const i
     const long waves = frags * (digits >= 4 ? 2 : 1);
     if ((waves + 3) / 4 > 0x7FFFFFFF) return hipErrorInvalidValue;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
-#define O2M_RES(M, T, DD, SC)                                                                    \
-    residue_kernel<M, T, DD, SC><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k,     \
-                                                        g.rows_pad, g.kblocks, g.plane_kblocks,   \
-                                                        g.kofs_p, g.kofs_m, g.plane_bytes, rp,    \
-                                                        planes)
-#define O2M_RES_D(M, T)                                       \
+    // complex fp32 entries in 16-byte pairs when every pair is aligned: along
+    // a column of B (k-chunks start at even k) or across rows 2i, 2i + 1 of A
+    // (lane chunks of one row, up to three digits); an even ld and a 16-byte
+    // aligned base suffice
+    const bool pairs = et == kF32 && (mode == 1 || digits <= 3) && ld % 2 == 0 && ((uintptr_t)X & 15) == 0;
+#define O2M_RES(M, T, DD, SC, PR)                                                                \
+    residue_kernel<M, T, DD, SC, PR><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k, \
+                                                            g.rows_pad, g.kblocks, g.plane_kblocks, \
+                                                            g.kofs_p, g.kofs_m, g.plane_bytes, rp,  \
+                                                            planes)
+#define O2M_RES_D(M, T, PR)                                   \
     switch (digits) {                                         \
-    case 1: O2M_RES(M, T, 1, true); break;                    \
-    case 2: O2M_RES(M, T, 2, true); break;                    \
-    case 3: O2M_RES(M, T, 3, true); break;                    \
-    case 4: O2M_RES(M, T, 4, true); break;                    \
-    case 5: O2M_RES(M, T, 5, true); break;                    \
+    case 1: O2M_RES(M, T, 1, true, PR); break;                \
+    case 2: O2M_RES(M, T, 2, true, PR); break;                \
+    case 3: O2M_RES(M, T, 3, true, PR); break;                \
+    case 4: O2M_RES(M, T, 4, true, PR); break;                \
+    case 5: O2M_RES(M, T, 5, true, PR); break;                \
     default: return hipErrorInvalidValue;                     \
     }
-    if (mode == 0 && et == kF64) { O2M_RES_D(0, kF64) }
-    else if (mode == 1 && et == kF64) { O2M_RES_D(1, kF64) }
-    else if (mode == 0 && et == kF32) { O2M_RES_D(0, kF32) }
-    else if (mode == 1 && et == kF32) { O2M_RES_D(1, kF32) }
-    else if (mode == 2 && et == kR64) { O2M_RES_D(2, kR64) }
-    else if (mode == 0 && et == kI32) O2M_RES(0, kI32, 2, false);
-    else if (mode == 1 && et == kI32) O2M_RES(1, kI32, 2, false);
+    if (mode == 0 && et == kF64) { O2M_RES_D(0, kF64, false) }
+    else if (mode == 1 && et == kF64) { O2M_RES_D(1, kF64, false) }
+    else if (mode == 0 && et == kF32 && pairs) {
+        switch (digits) {
+        case 1: O2M_RES(0, kF32, 1, true, true); break;
+        case 2: O2M_RES(0, kF32, 2, true, true); break;
+        case 3: O2M_RES(0, kF32, 3, true, true); break;
+        default: return hipErrorInvalidValue;
+        }
+    }
+    else if (mode == 0 && et == kF32) { O2M_RES_D(0, kF32, false) }
+    else if (mode == 1 && et == kF32 && pairs) { O2M_RES_D(1, kF32, true) }
+    else if (mode == 1 && et == kF32) { O2M_RES_D(1, kF32, false) }
+    else if (mode == 2 && et == kR64) { O2M_RES_D(2, kR64, false) }
+    else if (mode == 0 && et == kI32) O2M_RES(0, kI32, 2, false, false);
+    else if (mode == 1 && et == kI32) O2M_RES(1, kI32, 2, false, false);
     else return hipErrorInvalidValue;
 #undef O2M_RES_D
 #undef O2M_RES

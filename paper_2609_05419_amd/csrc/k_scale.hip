@@ -199,18 +199,38 @@ __global__ __launch_bounds__(256) void cs_scan_rows(int rows, int cols, const vo
 
 // Column mode (columns of a column-major X, contiguous): a workgroup covers
 // kColChunk entries of one column, kBatch per thread, held while the
-// workgroup agrees on the chunk maximum.
-template <ElemType ET>
+// workgroup agrees on the chunk maximum.  PAIRS: complex fp32 entries are
+// read two per 16-byte load (the host sets it when every pair is aligned).
+template <ElemType ET, bool PAIRS = false>
 __global__ __launch_bounds__(256) void cs_scan_cols(int rows, int cols, const void *X, int ld, CsPartials p) {
     const int c = blockIdx.x;
     const int r0 = blockIdx.y * kColChunk;
     const int r1 = min(rows, r0 + kColChunk);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     typename Raw<ET>::T x[kBatch];
+    if constexpr (PAIRS) {
+        static_assert(ET == kF32, "pairs of complex fp32 entries");
+        const float2 *Xc = reinterpret_cast<const float2 *>(X) + (size_t)c * ld;
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-        const int r = r0 + threadIdx.x + 256 * u;
-        x[u] = r < r1 ? Raw<ET>::load(X, (size_t)r + (size_t)c * ld) : Raw<ET>::zero();
+        for (int u = 0; u < kBatch / 2; ++u) {
+            const int r = r0 + 2 * threadIdx.x + 512 * u;
+            float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (r + 1 < r1) {
+                v = *reinterpret_cast<const float4 *>(Xc + r);
+            } else if (r < r1) {
+                const float2 t = Xc[r];
+                v.x = t.x;
+                v.y = t.y;
+            }
+            x[2 * u] = make_float2(v.x, v.y);
+            x[2 * u + 1] = make_float2(v.z, v.w);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int r = r0 + threadIdx.x + 256 * u;
+            x[u] = r < r1 ? Raw<ET>::load(X, (size_t)r + (size_t)c * ld) : Raw<ET>::zero();
+        }
     }
     unsigned long long best = 0;
 #pragma unroll
@@ -495,7 +515,11 @@ hipError_t launch_cs_scan(int mode, ElemType et, int rows, int cols, const void 
         dim3 grid(cols, (rows + kColChunk - 1) / kColChunk);
         switch (et) {
         case kF64: cs_scan_cols<kF64><<<grid, 256, 0, st>>>(rows, cols, X, ld, p); break;
-        case kF32: cs_scan_cols<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, p); break;
+        case kF32:
+            // chunks start at even rows: an even ld and a 16-byte aligned base align every pair
+            if (ld % 2 == 0 && ((uintptr_t)X & 15) == 0) cs_scan_cols<kF32, true><<<grid, 256, 0, st>>>(rows, cols, X, ld, p);
+            else cs_scan_cols<kF32><<<grid, 256, 0, st>>>(rows, cols, X, ld, p);
+            break;
         case kR64: cs_scan_cols<kR64><<<grid, 256, 0, st>>>(rows, cols, X, ld, p); break;
         default: return hipErrorInvalidValue;
         }

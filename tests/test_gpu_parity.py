@@ -577,6 +577,37 @@ def test_zherk_dsyrk_ragged_padded_ldc(o2m, n, N):
     assert same_bits(gotr[:n, :][low], O.oq_dsyrk(r, N)[low])
     assert (gotr[:n, :][~low] == -4.25).all() and (gotr[n:, :] == -4.25).all()
 
+def _offset_view(x, pad_rows, offset):
+    """As _padded_view, with the view starting `offset` elements into the
+    buffer (a base address off the 16-byte grid for offset 1 in fp32)."""
+    rows, cols = x.shape
+    big = np.full((rows + pad_rows, cols), np.nan, dtype=x.dtype)
+    big[offset:offset + rows, :] = x
+    return to_dev(big)[offset:offset + rows, :]
+
+
+# complex fp32 entries are read two per 16-byte load when every pair is
+# aligned (even leading dimension, aligned base): consecutive entries of a
+# column of B, rows 2i, 2i + 1 of A; one entry per load otherwise
+PAIR_CASES = [(41, 33, 11, 0), (41, 33, 10, 0), (40, 33, 11, 1), (41, 4101, 3, 0), (40, 4101, 4, 1), (257, 300, 5, 0)]
+
+
+@pytest.mark.parametrize("rule", ["max", "cs"])
+@pytest.mark.parametrize("m,k,pad,offset", PAIR_CASES, ids=[f"m{m}-k{k}-pad{p}-off{o}" for m, k, p, o in PAIR_CASES])
+def test_cgemm_paired_and_single_loads(o2m, m, k, pad, offset, rule):
+    a = W.complex_matrix(m, k, 415, dist="uniform", dtype=np.complex64)
+    b = W.complex_matrix(k, 21, 416, dist="uniform", dtype=np.complex64)
+    B = _offset_view(b, pad, offset)
+    assert B.stride(1) == k + pad
+    got = host(o2m.cgemm_2m(to_dev(a), B, n_moduli=8, scaling=rule))
+    ref = O.oq_cgemm(a, b, 8, scaling=rule)
+    assert same_bits(got, ref)
+    A = _offset_view(a, pad, offset)                  # A's rows in pairs (or not), B plain
+    assert A.stride(1) == m + pad
+    got = host(o2m.cgemm_2m(A, to_dev(b), n_moduli=8, scaling=rule))
+    assert same_bits(got, ref)
+
+
 def test_cgemm_and_zherk_strided(o2m):
     a = W.complex_matrix(40, 33, 411, dist="uniform", dtype=np.complex64)
     b = W.complex_matrix(33, 21, 412, dist="uniform", dtype=np.complex64)

@@ -347,3 +347,28 @@ def test_cs_resummed_rows_symmetric_calls(o2m):
     ref = O.oq_dsyrk(r, N, scaling="cs")
     got = host(o2m.dsyrk_2m(to_dev(r), n_moduli=N, scaling="cs"))
     assert same_bits(got[LOW(n)], ref[LOW(n)])
+
+
+@pytest.mark.slow
+def test_cs_k_at_the_int32_limit_sampled(o2m):
+    """k = 149130 under the Cauchy-Schwarz rule: 1166 chunk records per row of
+    A, 73 per column of B, rows and columns among them that the records leave
+    open; exponents equal the oracle's, sampled entries bit-exact."""
+    from cs_inputs import straddle_vector
+    m, n, k, N = 256, 300, 149130, 16
+    a = W.complex_matrix(m, k, 441, dist="phi", phi=2.0)
+    b = W.complex_matrix(k, n, 442, dist="phi", phi=2.0)
+    a[17, :] = straddle_vector(k, "low")
+    a[m - 1, :] = straddle_vector(k, "high")
+    b[:, 5] = straddle_vector(k, "high", exact=(0, 2048), binade=(2048, 2112), stride=2048)
+    _, E, F = o2m.zgemm_2m_residues(to_dev(a), to_dev(b), n_moduli=N, scaling="cs")
+    E0, _, F0, _ = O.exponents(a, b, "cs")
+    assert np.array_equal(E.cpu().numpy(), E0) and np.array_equal(F.cpu().numpy(), F0)
+    C = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N, scaling="cs"))
+    rng = np.random.default_rng(27)
+    ent = [(0, 0), (m - 1, n - 1), (17, 5), (m - 1, 5)]
+    ent += [(int(i), int(j)) for i, j in zip(rng.integers(0, m, 28), rng.integers(0, n, 28))]
+    got = np.array([C[i, j] for i, j in ent])
+    ok = same_bits(got, O.oq_zgemm(a, b, N, entries=ent, scaling="cs"))
+    report("cs k=149130", bitexact=ok)
+    assert ok
