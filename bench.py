@@ -211,6 +211,18 @@ def error_curve() -> int:
     def to_dev(x):
         return torch.from_numpy(np.ascontiguousarray(x.T)).to(dev).t()
 
+    ta, tb = args.transa, args.transb
+    if (ta, tb) != ("N", "N") and op not in ("zgemm", "cgemm"):
+        print("--transa/--transb apply to zgemm and cgemm only", file=sys.stderr)
+        return 2
+
+    def stored(x, t):
+        """The device matrix a caller stores for the operand x under op t."""
+        return to_dev(x if t == "N" else (x.T if t == "T" else x.conj().T))
+
+    def op_view(X, t):
+        return X if t == "N" else (X.mT if t == "T" else X.mH)
+
     m = n = k = 1024
     sa, sb = workloads.config_seeds(2)
     for op, dist, dtype, u, Ns in (("zgemm", "normal", np.complex128, 2.0 ** -53, range(6, 23, 2)),
@@ -263,6 +275,10 @@ def main() -> int:
     ap.add_argument("--n", type=int, default=8192)
     ap.add_argument("--k", type=int, default=8192)
     ap.add_argument("--n-moduli", type=int, default=16)
+    ap.add_argument("--transa", choices=["N", "T", "C"], default="N",
+                    help="zgemm/cgemm: the stored A is op(A) itself, its transpose or its conjugate "
+                         "transpose (zgemm_2m_op); the product is the same")
+    ap.add_argument("--transb", choices=["N", "T", "C"], default="N")
     ap.add_argument("--phi", type=float, default=0.5)
     ap.add_argument("--accuracy-samples", type=int, default=1024,
                     help="output entries compared with the double-double reference (and native matmul)")
@@ -309,6 +325,18 @@ def main() -> int:
     def to_dev(x):
         return torch.from_numpy(np.ascontiguousarray(x.T)).to(dev).t()
 
+    ta, tb = args.transa, args.transb
+    if (ta, tb) != ("N", "N") and op not in ("zgemm", "cgemm"):
+        print("--transa/--transb apply to zgemm and cgemm only", file=sys.stderr)
+        return 2
+
+    def stored(x, t):
+        """The device matrix a caller stores for the operand x under op t."""
+        return to_dev(x if t == "N" else (x.T if t == "T" else x.conj().T))
+
+    def op_view(X, t):
+        return X if t == "N" else (X.mT if t == "T" else X.mH)
+
     cfg = {"zgemm": 3, "cgemm": 4, "zherk": 5, "dsyrk": 5, "zher2k": 5, "dsyr2k": 5}[op]
     sa, sb = workloads.config_seeds(cfg)
     log(f"bench: {op} m={m} n={n} k={k} N={N}: generating inputs")
@@ -316,9 +344,12 @@ def main() -> int:
     if op == "zgemm":
         a = workloads.complex_matrix(m, k, sa, dist="phi", phi=args.phi)
         b = workloads.complex_matrix(k, n, sb, dist="phi", phi=args.phi)
-        A, B = to_dev(a), to_dev(b)
+        A, B = stored(a, ta), stored(b, tb)
         C = torch.empty((n, m), dtype=torch.complex128, device=dev).t()
-        call = lambda N: o2m.zgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        if (ta, tb) == ("N", "N"):
+            call = lambda N: o2m.zgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        else:
+            call = lambda N: o2m.zgemm_2m_op(A, B, ta, tb, n_moduli=N, out=C, scaling=rule)
         flops, int8_per_n = 8.0 * m * n * k, 4.0 * m * n * k
         metric = ("effective ZGEMM TFLOP/s (8mnk/t) at m=n=k=8192 + int8 MFMA util %"
                   if (m, n, k) == (8192, 8192, 8192) else "effective ZGEMM TFLOP/s (8mnk/t)")
@@ -330,9 +361,12 @@ def main() -> int:
     elif op == "cgemm":
         a = workloads.complex_matrix(m, k, sa, dist="uniform", dtype=np.complex64)
         b = workloads.complex_matrix(k, n, sb, dist="uniform", dtype=np.complex64)
-        A, B = to_dev(a), to_dev(b)
+        A, B = stored(a, ta), stored(b, tb)
         C = torch.empty((n, m), dtype=torch.complex64, device=dev).t()
-        call = lambda N: o2m.cgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        if (ta, tb) == ("N", "N"):
+            call = lambda N: o2m.cgemm_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        else:
+            call = lambda N: o2m.cgemm_2m_op(A, B, ta, tb, n_moduli=N, out=C, scaling=rule)
         flops, int8_per_n = 8.0 * m * n * k, 4.0 * m * n * k
         metric = "effective CGEMM TFLOP/s (8mnk/t)"
         desc = f"cgemm_2m {m}x{n}x{k} complex64, parts U(-1,1), {{N}} 2M moduli, int8 MFMA"
@@ -415,7 +449,8 @@ def main() -> int:
         # int8 work: 2 GEMMs per 2M modulus; a hybrid set's 3M moduli take 3
         n2, n3 = min(N, 22), max(N - 22, 0)
         achieved = (n2 + 1.5 * n3) * int8_per_n / (gemm_ms * 1e-3) / 1e12
-        workload_key = f"{op} m{m} n{n} k{k} N{N} phi{args.phi}" + ("" if rule == "max" else f" {rule}")
+        workload_key = (f"{op} m{m} n{n} k{k} N{N} phi{args.phi}" + ("" if rule == "max" else f" {rule}")
+                        + ("" if (ta, tb) == ("N", "N") else f" op{ta}{tb}"))
         roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_INT8_TOPS,
                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
                     "traffic": load_traffic(workload_key)}
@@ -434,15 +469,16 @@ def main() -> int:
                                                     rng.integers(0, n, args.accuracy_samples))]
         if with_extras and not args.no_native and op in ("zgemm", "cgemm"):
             try:
+                An, Bn = op_view(A, ta), op_view(B, tb)
                 for _ in range(2):
-                    Cn = torch.matmul(A, B)
+                    Cn = torch.matmul(An, Bn)
                 torch.cuda.synchronize()
                 s2 = torch.cuda.Event(enable_timing=True)
                 e2 = torch.cuda.Event(enable_timing=True)
                 reps = 3
                 s2.record(stream)
                 for _ in range(reps):
-                    Cn = torch.matmul(A, B)
+                    Cn = torch.matmul(An, Bn)
                 e2.record(stream)
                 torch.cuda.synchronize()
                 nms = s2.elapsed_time(e2) / reps
@@ -519,6 +555,7 @@ def main() -> int:
             "data": "synthetic",
             "config": {"workload": desc.format(N=N), "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
                        "phi": args.phi if op == "zgemm" else None, "scaling_rule": rule,
+                       **({} if (ta, tb) == ("N", "N") else {"transa": ta, "transb": tb}),
                        "parallelism": "single GPU"},
             "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
             "int8_mfma_ceiling": ceiling,

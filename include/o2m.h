@@ -199,6 +199,24 @@ o2m_status zher2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const
 o2m_status dsyr2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
                         double *C, int ldc, int n_moduli, int scaling, void *stream);
 
+/* C = op(A) op(B) (Section 3.2, Algorithm 1, on the operands op(A), op(B)),
+   with op(X) = X for 'N', X^T for 'T' and X^H for 'C' (either case), BLAS
+   style: op(A) is m x k, stored as A (m x k, lda >= m) for 'N' or as an
+   k x m matrix (lda >= k) otherwise; op(B) is k x n, stored k x n (ldb >= k)
+   for 'N' or n x k (ldb >= n) otherwise.  Transposition and conjugation are
+   exact and no operand is copied: the kernels read rows of op(A) as columns
+   of the stored A when transposed, and conjugation negates imaginary parts as
+   they are read (it exchanges A+ and A- of eq. 2m-pre).  The result is that
+   of zgemm_2m_ex / cgemm_2m_ex on the explicitly formed op(A), op(B), bit for
+   bit.  Argument errors: -1 transa, -2 transb, -3 m, -4 n, -5 k, -6 A,
+   -7 lda, -8 B, -9 ldb, -10 C, -11 ldc. */
+o2m_status zgemm_2m_op(char transa, char transb, int m, int n, int k, const double *A, int lda,
+                       const double *B, int ldb, double *C, int ldc, int n_moduli, int scaling,
+                       void *stream);
+o2m_status cgemm_2m_op(char transa, char transb, int m, int n, int k, const float *A, int lda,
+                       const float *B, int ldb, float *C, int ldc, int n_moduli, int scaling,
+                       void *stream);
+
 /* Exact Gaussian-integer product (Section 2): A m x k and B k x n with int32
    (re, im) pairs, C m x n with int64 (re, im) pairs.  No scaling: 2M modulo
    N moduli with N <= 8 (M < 2^63).  Exact when every entry satisfies

@@ -18,7 +18,8 @@ import os
 import torch
 
 __all__ = [
-    "zgemm_2m", "zgemm_2m_noalloc", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
+    "zgemm_2m", "zgemm_2m_noalloc", "cgemm_2m", "zgemm_2m_op", "cgemm_2m_op", "zherk_2m", "dsyrk_2m",
+    "zher2k_2m", "dsyr2k_2m", "gauss_gemm_2m",
     "zgemm_2m_residues", "moduli", "budget", "shifts", "workspace_bytes", "set_workspace",
     "release_workspace", "get_status", "STATUS_OVERFLOW", "STATUS_NONFINITE", "phase_timing", "phase_times", "colmajor", "O2MError", "LIB_PATH", "SCALING",
 ]
@@ -39,6 +40,8 @@ _L.zher2k_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
 _L.dsyr2k_2m.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _P]
 _L.zgemm_2m_ex.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.cgemm_2m_ex.argtypes = [_I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.zgemm_2m_op.argtypes = [_C, _C, _I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
+_L.cgemm_2m_op.argtypes = [_C, _C, _I, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.zherk_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.dsyrk_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _I, _I, _P]
 _L.zher2k_2m_ex.argtypes = [_C, _I, _I, _P, _I, _P, _I, _P, _I, _I, _I, _P]
@@ -59,7 +62,7 @@ _L.o2m_phase_times.argtypes = [_P, _I]
 _L.o2m_status_string.argtypes = [_I]
 _L.o2m_status_string.restype = ctypes.c_char_p
 for _f in ("zgemm_2m", "zgemm_2m_noalloc", "cgemm_2m", "zherk_2m", "dsyrk_2m", "zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex",
-           "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex", "zher2k_2m_ex", "dsyr2k_2m_ex", "gauss_gemm_2m",
+           "cgemm_2m_ex", "zgemm_2m_op", "cgemm_2m_op", "zherk_2m_ex", "dsyrk_2m_ex", "zher2k_2m_ex", "dsyr2k_2m_ex", "gauss_gemm_2m",
            "zgemm_2m_residues", "zgemm_2m_residues_ex", "o2m_moduli", "o2m_budget", "o2m_shifts",
            "o2m_set_workspace", "o2m_release_workspace", "o2m_get_status", "o2m_phase_timing",
            "o2m_phase_times"):
@@ -98,6 +101,8 @@ def colmajor(x: torch.Tensor) -> torch.Tensor:
 def _ld(x: torch.Tensor) -> int:
     if x.dim() != 2:
         raise ValueError("expected a matrix")
+    if x.numel() == 0:
+        return max(x.size(0), 1)                 # nothing is read or written
     if x.size(0) > 1 and x.stride(0) != 1:
         raise ValueError("matrix must be column-major (stride(0) == 1); use colmajor()")
     return max(x.stride(1), x.size(0), 1)
@@ -162,6 +167,40 @@ def cgemm_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 8, out: torch.Ten
     _check(_L.cgemm_2m_ex(m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(), _ld(C),
                           n_moduli, _rule(scaling), _stream(stream)), "cgemm_2m")
     return C
+
+
+def _gemm_op(fn, name, A, B, transa, transb, dtype, n_moduli, out, stream, scaling):
+    for nm, x in (("A", A), ("B", B)):
+        if x.dtype != dtype:
+            raise TypeError(f"{nm} must be {dtype}, got {x.dtype}")
+        if not x.is_cuda:
+            raise ValueError(f"{nm} must be a device tensor")
+    ta, tb = transa.upper(), transb.upper()
+    if ta not in ("N", "T", "C") or tb not in ("N", "T", "C"):
+        raise ValueError(f"transa, transb must be 'N', 'T' or 'C', got {transa!r}, {transb!r}")
+    m, k = A.shape if ta == "N" else (A.size(1), A.size(0))
+    kb, n = B.shape if tb == "N" else (B.size(1), B.size(0))
+    if k != kb:
+        raise ValueError(f"inner dimensions differ: op(A) {m} x {k}, op(B) {kb} x {n}")
+    C = _empty_colmajor(m, n, dtype, A.device) if out is None else out
+    _check(fn(ta.encode(), tb.encode(), m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
+              _ld(C), n_moduli, _rule(scaling), _stream(stream)), name)
+    return C
+
+
+def zgemm_2m_op(A: torch.Tensor, B: torch.Tensor, transa: str = "N", transb: str = "N", n_moduli: int = 16,
+                out: torch.Tensor | None = None, stream=None, scaling: str = "max") -> torch.Tensor:
+    """C = op(A) op(B) for complex128 tensors, op = 'N' (as is), 'T'
+    (transpose) or 'C' (conjugate transpose); A and B as stored (column-major)."""
+    return _gemm_op(_L.zgemm_2m_op, "zgemm_2m_op", A, B, transa, transb, torch.complex128, n_moduli, out, stream,
+                    scaling)
+
+
+def cgemm_2m_op(A: torch.Tensor, B: torch.Tensor, transa: str = "N", transb: str = "N", n_moduli: int = 8,
+                out: torch.Tensor | None = None, stream=None, scaling: str = "max") -> torch.Tensor:
+    """As zgemm_2m_op for complex64 tensors (result rounded once to fp32)."""
+    return _gemm_op(_L.cgemm_2m_op, "cgemm_2m_op", A, B, transa, transb, torch.complex64, n_moduli, out, stream,
+                    scaling)
 
 
 def _sym_out(out, n, dtype, device):

@@ -8,6 +8,7 @@
 //   K3  batched int8 MFMA GEMMs, C mod m as int8       (step 4, eq. 2m-mul)
 //   K4  2M post, CRT, symmetric lift, descale          (steps 4-7, eq. 2m-post)
 // and returns without synchronizing.
+#include <algorithm>
 #include <atomic>
 #include <map>
 #include <math.h>
@@ -113,8 +114,10 @@ Geometry make_geometry(int rows_a, int rows_b, int k, int N, bool sym, int halve
     g.planes = sym ? 2 * N : g.products;
     g.shared_planes = sym;
     g.kscan = kscan;
-    g.cs_ca = cs_chunks(0, rows_a, kscan);
-    g.cs_cb = sym ? 0 : cs_chunks(1, kscan, rows_b);
+    // room for either layout of a GEMM operand (rows of a column-major matrix,
+    // or columns when it is transposed); symmetric ops read rows only
+    g.cs_ca = sym ? cs_chunks(0, rows_a, kscan) : std::max(cs_chunks(0, rows_a, kscan), cs_chunks(1, kscan, rows_a));
+    g.cs_cb = sym ? 0 : std::max(cs_chunks(1, kscan, rows_b), cs_chunks(0, rows_b, kscan));
     return g;
 }
 
@@ -275,6 +278,7 @@ struct Call {
     int8_t *res_out;
     int32_t *E_out, *F_out;
     bool noalloc = false;     // workspace = the static scratch array
+    char ta = 'N', tb = 'N';  // GEMM operands: op(X) = X, X^T or X^H ('N', 'T', 'C')
 };
 
 bool is_sym(Op op) { return op == kOpH || op == kOpS || op == kOpH2 || op == kOpS2; }
@@ -333,12 +337,20 @@ o2m_status run(const Call &c) {
     // fill over the contiguous amax_a .. queue region of the workspace (carve
     // order)
     O2M_TRY(launch_zero(b.amax_a, (size_t)((char *)b.E - (char *)b.amax_a), c.st));
+    // where the operand rows sit: A's rows are rows of the stored A (mode 0)
+    // or, transposed, its columns (mode 1); B's operand rows (the columns of
+    // op(B)) are columns of the stored B (mode 1) or, transposed, its rows
+    const int amode = c.ta == 'N' ? 0 : 1, bmode = c.tb == 'N' ? 1 : 0;
+    const int a_rows = amode == 0 ? c.m : c.k, a_cols = amode == 0 ? c.k : c.m;  // stored A
+    const int b_rows = bmode == 1 ? c.k : c.n, b_cols = bmode == 1 ? c.n : c.k;  // stored B
     if (cs && c.op != kOpG) {
         // one pass over each operand: chunk records, then the exponents they
         // settle (the few entries they leave open are summed from the data)
-        O2M_TRY(launch_cs_scan(0, et, c.m, c.k, c.A, c.lda, b.csa, 0, c.st));
-        if (two) O2M_TRY(launch_cs_scan(0, et, c.m, c.k, c.B, c.ldb, b.csa, g.cs_ca, c.st));
-        if (!sym) O2M_TRY(launch_cs_scan(1, et, c.k, c.n, c.B, c.ldb, b.csb, 0, c.st));
+        b.csa.chunks = cs_chunks(amode, a_rows, a_cols) * g.halves;
+        b.csb.chunks = sym ? 0 : cs_chunks(bmode, b_rows, b_cols);
+        O2M_TRY(launch_cs_scan(amode, et, a_rows, a_cols, c.A, c.lda, b.csa, 0, c.st));
+        if (two) O2M_TRY(launch_cs_scan(0, et, c.m, c.k, c.B, c.ldb, b.csa, b.csa.chunks / 2, c.st));
+        if (!sym) O2M_TRY(launch_cs_scan(bmode, et, b_rows, b_cols, c.B, c.ldb, b.csb, 0, c.st));
         CsCombineArgs cg;
         memset(&cg, 0, sizeof cg);
         cg.ca = c.m;
@@ -355,11 +367,13 @@ o2m_status run(const Call &c) {
         cg.B = sym ? nullptr : c.B;
         cg.ldb = c.ldb;
         cg.k = c.k;
+        cg.amode = amode;
+        cg.bmode = bmode;
         O2M_TRY(launch_cs_combine(et, cg, c.st));
     } else {
-        O2M_TRY(launch_amax(0, et, c.m, c.k, c.A, c.lda, b.amax_a, c.st));
+        O2M_TRY(launch_amax(amode, et, a_rows, a_cols, c.A, c.lda, b.amax_a, c.st));
         if (two) O2M_TRY(launch_amax(0, et, c.m, c.k, c.B, c.ldb, b.amax_a, c.st));
-        if (!sym) O2M_TRY(launch_amax(1, et, c.k, c.n, c.B, c.ldb, b.amax_b, c.st));
+        if (!sym) O2M_TRY(launch_amax(bmode, et, b_rows, b_cols, c.B, c.ldb, b.amax_b, c.st));
         if (c.op != kOpG)
             O2M_TRY(launch_exponents(c.m, b.amax_a, b.E, sym ? 0 : c.n, b.amax_b, b.F, status, c.st));
     }
@@ -370,10 +384,10 @@ o2m_status run(const Call &c) {
     // one GEMM per modulus gives C+ = A+ B-^T + B+ A-^T (Section 5, HER2K).
     const int kb = g.kblocks;
     const int pkb = g.halves * kb;
-    const int rmode = is_real_split(c.op) ? 2 : 0;
+    const int rmode = is_real_split(c.op) ? 2 : amode;
     const int khalf = is_real_split(c.op) ? kc : 0;
     const int32_t *Eq = c.op == kOpG ? nullptr : b.E;
-    PlaneGeom ga = {c.m, kc, c.k, g.a_pad, kb, pkb, 0, two ? kb : 0, g.plane_a};
+    PlaneGeom ga = {c.m, kc, c.k, g.a_pad, kb, pkb, 0, two ? kb : 0, g.plane_a, c.ta == 'C'};
     O2M_TRY(launch_residues(rmode, et, c.A, c.lda, Eq, pA, digits(c.scaling, pA), khalf, ga, t->res,
                             b.planes_a, c.st));
     if (two) {
@@ -382,8 +396,8 @@ o2m_status run(const Call &c) {
                                 b.planes_a, c.st));
     }
     if (!sym) {
-        PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, kb, kb, 0, 0, g.plane_b};
-        O2M_TRY(launch_residues(1, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, digits(c.scaling, pB), 0,
+        PlaneGeom gb = {c.n, c.k, c.k, g.b_pad, kb, kb, 0, 0, g.plane_b, c.tb == 'C'};
+        O2M_TRY(launch_residues(bmode, et, c.B, c.ldb, c.op == kOpG ? nullptr : b.F, pB, digits(c.scaling, pB), 0,
                                 gb, t->res, b.planes_b, c.st));
     }
     phase_mark(slot, 2, c.st);
@@ -507,6 +521,60 @@ o2m_status check_scaling(int scaling) {
     return scaling == O2M_SCALE_MAX || scaling == O2M_SCALE_CS ? O2M_OK : O2M_ERR_SCALING;
 }
 
+bool op_of(char op, Op *out) {
+    switch (op) {
+    case 'z': *out = kOpZ; return true;
+    case 'c': *out = kOpC; return true;
+    case 'h': *out = kOpH; return true;
+    case 's': *out = kOpS; return true;
+    case 'g': *out = kOpG; return true;
+    case 'r': *out = kOpR; return true;
+    case 'x': *out = kOpH2; return true;
+    case 'y': *out = kOpS2; return true;
+    default: return false;
+    }
+}
+
+// 'N', 'T' or 'C' (either case) as upper case; 0 for anything else
+char trans_of(char t) {
+    switch (t) {
+    case 'n': case 'N': return 'N';
+    case 't': case 'T': return 'T';
+    case 'c': case 'C': return 'C';
+    default: return 0;
+    }
+}
+
+o2m_status check_gemm_op(char ta, char tb, int m, int n, int k, const void *A, int lda, const void *B, int ldb,
+                         const void *C, int ldc, int N, int maxN) {
+    if (!trans_of(ta)) return -1;
+    if (!trans_of(tb)) return -2;
+    if (m < 0) return -3;
+    if (n < 0) return -4;
+    if (k < 0) return -5;
+    const int arows = trans_of(ta) == 'N' ? m : k, brows = trans_of(tb) == 'N' ? k : n;
+    if (!A && m > 0 && k > 0) return -6;
+    if (lda < (arows > 1 ? arows : 1)) return -7;
+    if (!B && k > 0 && n > 0) return -8;
+    if (ldb < (brows > 1 ? brows : 1)) return -9;
+    if (!C && m > 0 && n > 0) return -10;
+    if (ldc < (m > 1 ? m : 1)) return -11;
+    if (N < 1 || N > maxN) return O2M_ERR_NMODULI;
+    if (k > (N > O2M_MAX_MODULI ? O2M_MAX_K_HYBRID : O2M_MAX_K)) return O2M_ERR_KLIMIT;
+    return O2M_OK;
+}
+
+o2m_status gemm_op(Op op, char transa, char transb, int m, int n, int k, const void *A, int lda, const void *B,
+                   int ldb, void *C, int ldc, int n_moduli, int scaling, void *stream) {
+    o2m_status s = check_gemm_op(transa, transb, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_MAX_MODULI_HYBRID);
+    if (s == O2M_OK) s = check_scaling(scaling);
+    if (s != O2M_OK || m == 0 || n == 0) return s;
+    Call c{op, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr, nullptr, nullptr};
+    c.ta = trans_of(transa);
+    c.tb = trans_of(transb);
+    return run(c);
+}
+
 }  // namespace
 
 extern "C" {
@@ -533,6 +601,16 @@ o2m_status zgemm_2m_noalloc(int m, int n, int k, const double *A, int lda, const
 o2m_status zgemm_2m(int m, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
                     int ldc, int n_moduli, void *stream) {
     return zgemm_2m_ex(m, n, k, A, lda, B, ldb, C, ldc, n_moduli, O2M_SCALE_MAX, stream);
+}
+
+o2m_status zgemm_2m_op(char transa, char transb, int m, int n, int k, const double *A, int lda, const double *B,
+                       int ldb, double *C, int ldc, int n_moduli, int scaling, void *stream) {
+    return gemm_op(kOpZ, transa, transb, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, stream);
+}
+
+o2m_status cgemm_2m_op(char transa, char transb, int m, int n, int k, const float *A, int lda, const float *B,
+                       int ldb, float *C, int ldc, int n_moduli, int scaling, void *stream) {
+    return gemm_op(kOpC, transa, transb, m, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, stream);
 }
 
 o2m_status cgemm_2m_ex(int m, int n, int k, const float *A, int lda, const float *B, int ldb, float *C,
@@ -645,21 +723,6 @@ o2m_status o2m_budget(int n_moduli, int k, int *P_out) {
     return O2M_OK;
 }
 
-namespace {
-bool op_of(char op, Op *out) {
-    switch (op) {
-    case 'z': *out = kOpZ; return true;
-    case 'c': *out = kOpC; return true;
-    case 'h': *out = kOpH; return true;
-    case 's': *out = kOpS; return true;
-    case 'g': *out = kOpG; return true;
-    case 'r': *out = kOpR; return true;
-    case 'x': *out = kOpH2; return true;
-    case 'y': *out = kOpS2; return true;
-    default: return false;
-    }
-}
-}  // namespace
 
 o2m_status o2m_shifts(char op, int n_moduli, int k, int scaling, int *pA_out, int *pB_out) {
     Op o;

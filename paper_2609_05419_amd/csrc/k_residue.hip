@@ -100,6 +100,7 @@ __device__ inline void store_words(int8_t *dst, const uint32_t (&w)[PT / 4]) {
 // MODE 0: rows of X (A, column-major m x k): entry (r, kk) at X[r + kk*ld]
 // MODE 1: columns of X (B, column-major k x n): entry (r, kk) at X[kk + r*ld]
 // MODE 2: SYRK, X real column-major n x k: (r, kk) = X[r + kk ld] + i X[r + (kk+kh) ld]
+// conj: the operand is the complex conjugate of X (imaginary parts negated)
 // D: base-2^26 digits of the quantized values (1..5, from their bound)
 // PAIRS (complex fp32, the host sets it when every pair is 16-byte aligned):
 // MODE 1 reads two consecutive entries of a column of B per 16-byte load;
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
                                                       int shift, int khalf, int kreal, int rows, int k,
                                                       int rows_pad, int kblocks, int plane_kblocks,
                                                       int kofs_p, int kofs_m, size_t plane_bytes,
-                                                      ResidueParams rp, int8_t *planes) {
+                                                      int conj, ResidueParams rp, int8_t *planes) {
     constexpr int PT = per_thread<D>();
     constexpr int kHalves = 16 / PT;                          // waves per fragment
     const int lane = threadIdx.x & 63;
@@ -143,6 +144,7 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
     }
     auto put = [&](int e, double vr, double vi) {
         if (!live) vr = vi = 0.0;
+        if (conj) vi = -vi;                  // conjugated operand: exact
         if (SCALED) {
             vr = rint(ldexp(vr, sh));
             vi = rint(ldexp(vi, sh));
@@ -303,7 +305,7 @@ hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const i
 #define O2M_RES(M, T, DD, SC, PR)                                                                \
     residue_kernel<M, T, DD, SC, PR><<<blocks, 256, 0, st>>>(X, ld, E, shift, khalf, kreal, g.rows, g.k, \
                                                             g.rows_pad, g.kblocks, g.plane_kblocks, \
-                                                            g.kofs_p, g.kofs_m, g.plane_bytes, rp,  \
+                                                            g.kofs_p, g.kofs_m, g.plane_bytes, g.conj, rp, \
                                                             planes)
 #define O2M_RES_D(M, T, PR)                                   \
     switch (digits) {                                         \

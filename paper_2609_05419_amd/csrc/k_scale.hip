@@ -286,8 +286,9 @@ constexpr int kCombineWaves = 16;
 // E = the max exponent over the chunks (INT32_MIN for Inf/NaN, which also sets
 // kStatusNonfinite; 0 for a zero row), then the bracket of U from the chunk
 // records settles G = E - 20 + d.  A row whose bracket straddles a power of 4
-// is summed again from the data by the whole workgroup (rows: row i of A, and
-// of B2 for rank-2k updates; columns: column j of B) against E.
+// is summed again from the data by the whole workgroup (row i of A, and of B2
+// for rank-2k updates; column j of B; with transposed operands, a column of
+// the stored A or a row of the stored B) against E.
 template <ElemType ET>
 __global__ __launch_bounds__(64 * kCombineWaves) void cs_combine_kernel(CsCombineArgs g) {
     const int ba = (g.ca + 63) / 64;
@@ -368,13 +369,12 @@ __global__ __launch_bounds__(64 * kCombineWaves) void cs_combine_kernel(CsCombin
 #pragma unroll
             for (int q = 0; q < Raw<ET>::n; ++q) acc += ssq_term(v[q], er);
         };
+        const void *X = side_a ? g.A : g.B;
+        const int ld = side_a ? g.lda : g.ldb;
+        const bool as_rows = (side_a ? g.amode : g.bmode) == 0;
         for (int c = threadIdx.x; c < g.k; c += 64 * kCombineWaves) {
-            if (side_a) {
-                add(Raw<ET>::load(g.A, (size_t)r + (size_t)c * g.lda));
-                if (g.B2) add(Raw<ET>::load(g.B2, (size_t)r + (size_t)c * g.ldb2));
-            } else {
-                add(Raw<ET>::load(g.B, (size_t)c + (size_t)r * g.ldb));
-            }
+            add(Raw<ET>::load(X, as_rows ? (size_t)r + (size_t)c * ld : (size_t)c + (size_t)r * ld));
+            if (side_a && g.B2) add(Raw<ET>::load(g.B2, (size_t)r + (size_t)c * g.ldb2));
         }
         for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
         if (lane == 0) sm[w][0] = acc;

@@ -157,7 +157,10 @@ struct CsCombineArgs {
     int *status;
     const void *A, *B2, *B;
     int lda, ldb2, ldb;
-    int k;                  // columns of A (rows of B)
+    int k;                  // entries per row of A (per column of B)
+    int amode, bmode;       // how the entries sit in memory: 0 = a row of a
+                            // column-major matrix (A's default), 1 = a column
+                            // (B's default); B2 (rank-2k) is read as rows
 };
 hipError_t launch_cs_combine(ElemType et, const CsCombineArgs &g, hipStream_t st);
 // K2: quantize + residues + 2M pre into operand planes.
@@ -177,6 +180,7 @@ struct PlaneGeom {
     int plane_kblocks;       // k-blocks of the destination planes
     int kofs_p, kofs_m;      // k-block offsets in the + and - planes
     size_t plane_bytes;  // rows_pad * plane_kblocks * 64
+    int conj;            // 1: the operand is conj(X) (a conjugate-transposed GEMM operand)
 };
 hipError_t launch_residues(int mode, ElemType et, const void *X, int ld, const int32_t *E, int shift,
                            int digits, int khalf, const PlaneGeom &g, const ResidueParams &rp,

@@ -68,9 +68,10 @@ def test_workspace_bytes_grow_with_the_problem():
     import paper_2609_05419_amd as o2m
     z = o2m.workspace_bytes("z", 8192, 8192, 8192, 16)
     # planes: 2N (m + n) k + 2N m n bytes, plus exponents and the
-    # Cauchy-Schwarz chunk records (24 bytes per row of A and 128 columns, per
-    # column of B and 2048 rows)
-    records = 24 * (8192 * (8192 // 128) + 8192 * (8192 // 2048))
+    # Cauchy-Schwarz chunk records: 24 bytes per operand row and chunk, with
+    # room for either layout of each GEMM operand (rows of a column-major
+    # matrix: chunks of 128 columns; columns: chunks of 2048 rows)
+    records = 24 * (8192 * (8192 // 128) + 8192 * (8192 // 128))
     assert z >= 32 * (8192 * 8192 * 3) + records
     assert z < 32 * (8192 * 8192 * 3) + records + (1 << 20)
     h = o2m.workspace_bytes("h", 8192, 8192, 8192, 16)
@@ -119,7 +120,7 @@ def test_argument_errors_are_reported_before_any_gpu_work(lib):
 def test_new_entry_points_declared():
     names = declared_functions()
     for f in ("zher2k_2m", "dsyr2k_2m", "zgemm_2m_ex", "cgemm_2m_ex", "zherk_2m_ex", "dsyrk_2m_ex",
-              "zher2k_2m_ex", "dsyr2k_2m_ex", "zgemm_2m_residues_ex", "o2m_shifts"):
+              "zher2k_2m_ex", "dsyr2k_2m_ex", "zgemm_2m_residues_ex", "o2m_shifts", "zgemm_2m_op", "cgemm_2m_op"):
         assert f in names
 
 
@@ -173,6 +174,31 @@ def test_rank2k_and_scaling_argument_errors(lib):
     assert lib.zgemm_2m_ex(4, 4, 8192, fake, 4, fake, 8192, fake, 4, 1, 1, None) == -26  # no CS shifts
     lib.o2m_status_string.restype = ctypes.c_char_p
     assert b"scaling" in lib.o2m_status_string(-26)
+
+
+def test_transposed_gemm_argument_errors(lib):
+    P, I, C = ctypes.c_void_p, ctypes.c_int, ctypes.c_char
+    fake = P(0x1000)
+    for f in (lib.zgemm_2m_op, lib.cgemm_2m_op):
+        f.argtypes = [C, C, I, I, I, P, I, P, I, P, I, I, I, P]
+        # op(A) 6 x 5 (stored 5 x 6 when transposed), op(B) 5 x 7 (stored 7 x 5)
+        assert f(b"X", b"N", 6, 7, 5, fake, 6, fake, 5, fake, 6, 16, 0, None) == -1
+        assert f(b"N", b"H", 6, 7, 5, fake, 6, fake, 5, fake, 6, 16, 0, None) == -2
+        assert f(b"N", b"N", -1, 7, 5, fake, 6, fake, 5, fake, 6, 16, 0, None) == -3
+        assert f(b"N", b"N", 6, -1, 5, fake, 6, fake, 5, fake, 6, 16, 0, None) == -4
+        assert f(b"N", b"N", 6, 7, -1, fake, 6, fake, 5, fake, 6, 16, 0, None) == -5
+        assert f(b"N", b"N", 6, 7, 5, None, 6, fake, 5, fake, 6, 16, 0, None) == -6
+        assert f(b"N", b"N", 6, 7, 5, fake, 5, fake, 5, fake, 6, 16, 0, None) == -7    # lda < m
+        assert f(b"T", b"N", 6, 7, 5, fake, 4, fake, 5, fake, 6, 16, 0, None) == -7    # lda < k
+        assert f(b"c", b"N", 6, 7, 5, fake, 4, fake, 5, fake, 6, 16, 0, None) == -7
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, None, 5, fake, 6, 16, 0, None) == -8
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, fake, 4, fake, 6, 16, 0, None) == -9    # ldb < k
+        assert f(b"N", b"T", 6, 7, 5, fake, 6, fake, 6, fake, 6, 16, 0, None) == -9    # ldb < n
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, fake, 5, None, 6, 16, 0, None) == -10
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, fake, 5, fake, 5, 16, 0, None) == -11
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, fake, 5, fake, 6, 33, 0, None) == -20
+        assert f(b"N", b"N", 6, 7, 5, fake, 6, fake, 5, fake, 6, 16, 5, None) == -26
+        assert f(b"t", b"c", 0, 7, 5, None, 5, fake, 7, None, 1, 16, 1, None) == 0   # empty: no-op
 
 
 def test_probe_library_exports_its_header():

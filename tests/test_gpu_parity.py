@@ -874,3 +874,79 @@ def test_residue_digit_boundaries(o2m, rule, N, k):
     ok = same_bits(got, ref)
     report("digit boundary", rule=rule, N=N, k=k, pA=pA, pB=pB, bitexact=ok)
     assert ok
+
+
+# --------------------------------------------- transposed and conjugated operands
+# C = op(A) op(B), op = 'N', 'T' or 'C': the library reads rows of op(A) as
+# columns of the stored A when transposed and negates imaginary parts when
+# conjugated; the result must equal the oracle's exact output on the explicitly
+# formed op(A), op(B).
+
+OPS = [(ta, tb) for ta in "NTC" for tb in "NTC"]
+
+
+def _stored(op_x, t):
+    """The matrix a caller stores so that op(stored) = op_x."""
+    return op_x if t == "N" else (op_x.T if t == "T" else op_x.conj().T)
+
+
+@pytest.mark.parametrize("rule", ["max", "cs"])
+@pytest.mark.parametrize("ta,tb", OPS, ids=[a + b for a, b in OPS])
+def test_zgemm_op_bit_exact(o2m, ta, tb, rule):
+    m, n, k, N = 70, 50, 90, 16
+    opa = W.complex_matrix(m, k, 4701, dist="phi", phi=2.0)
+    opb = W.complex_matrix(k, n, 4702, dist="phi", phi=2.0)
+    A = _padded_view(np.ascontiguousarray(_stored(opa, ta)), 5)
+    B = _padded_view(np.ascontiguousarray(_stored(opb, tb)), 3)
+    got = host(o2m.zgemm_2m_op(A, B, ta, tb, n_moduli=N, scaling=rule))
+    ok = same_bits(got, O.oq_zgemm(opa, opb, N, scaling=rule))
+    report("zgemm op", ops=ta + tb, rule=rule, bitexact=ok)
+    assert ok
+
+
+@pytest.mark.parametrize("rule", ["max", "cs"])
+@pytest.mark.parametrize("ta,tb,pad", [("T", "N", 4), ("C", "T", 3), ("N", "C", 2), ("C", "C", 1)])
+def test_cgemm_op_bit_exact(o2m, ta, tb, pad, rule):
+    m, n, k = 41, 30, 67
+    opa = W.complex_matrix(m, k, 4711, dist="uniform", dtype=np.complex64)
+    opb = W.complex_matrix(k, n, 4712, dist="uniform", dtype=np.complex64)
+    A = _padded_view(np.ascontiguousarray(_stored(opa, ta)), pad)
+    B = _padded_view(np.ascontiguousarray(_stored(opb, tb)), pad + 1)
+    got = host(o2m.cgemm_2m_op(A, B, ta, tb, n_moduli=8, scaling=rule))
+    assert same_bits(got, O.oq_cgemm(opa, opb, 8, scaling=rule))
+
+
+def test_zgemm_op_matches_plain_call_and_hybrid(o2m):
+    """'N','N' is the plain call; a hybrid set (N = 26) with both operands
+    conjugate-transposed; k = 0 zeroes C."""
+    m, n, k = 33, 29, 300
+    a = W.complex_matrix(m, k, 4721)
+    b = W.complex_matrix(k, n, 4722)
+    plain = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=16))
+    assert same_bits(host(o2m.zgemm_2m_op(to_dev(a), to_dev(b), "n", "n", n_moduli=16)), plain)
+    got = host(o2m.zgemm_2m_op(to_dev(a.conj().T), to_dev(b.conj().T), "C", "C", n_moduli=26, scaling="cs"))
+    assert same_bits(got, O.oq_zgemm(a, b, 26, scaling="cs"))
+    z = o2m.zgemm_2m_op(to_dev(np.zeros((0, m), np.complex128)), to_dev(np.zeros((n, 0), np.complex128)),
+                        "T", "T", n_moduli=16)
+    assert z.shape == (m, n) and (host(z) == 0).all()
+
+
+def test_cs_resummed_entries_transposed_operands(o2m):
+    """Rows of op(A) read as columns of the stored A, columns of op(B) read as
+    rows of the stored B, among them ones whose chunk records leave the
+    Cauchy-Schwarz exponent open (summed again from the data)."""
+    from cs_inputs import straddle_vector
+    m, n, k, N = 24, 20, 4096, 16
+    opa = W.complex_matrix(m, k, 4731, dist="phi", phi=0.5)
+    opb = W.complex_matrix(k, n, 4732, dist="phi", phi=0.5)
+    for i, kind in ((2, "low"), (m - 1, "high")):      # a column of the stored A: chunks of 2048
+        opa[i, :] = straddle_vector(k, kind, exact=(0, 2048), binade=(2048, 2112), stride=2048)
+    for j, kind in ((0, "high"), (11, "low")):         # a row of the stored B: chunks of 16..128 columns
+        opb[:, j] = straddle_vector(k, kind)
+    for ta, tb in (("T", "T"), ("C", "C"), ("C", "T")):
+        A = to_dev(np.ascontiguousarray(_stored(opa, ta)))
+        B = to_dev(np.ascontiguousarray(_stored(opb, tb)))
+        got = host(o2m.zgemm_2m_op(A, B, ta, tb, n_moduli=N, scaling="cs"))
+        ok = same_bits(got, O.oq_zgemm(opa, opb, N, scaling="cs"))
+        report("cs re-summed, transposed", ops=ta + tb, bitexact=ok)
+        assert ok
