@@ -279,6 +279,8 @@ def main() -> int:
                     help="zgemm/cgemm: the stored A is op(A) itself, its transpose or its conjugate "
                          "transpose (zgemm_2m_op); the product is the same")
     ap.add_argument("--transb", choices=["N", "T", "C"], default="N")
+    ap.add_argument("--uplo", choices=["L", "U"], default="L",
+                    help="zherk/dsyrk/zher2k/dsyr2k: the triangle written")
     ap.add_argument("--phi", type=float, default=0.5)
     ap.add_argument("--accuracy-samples", type=int, default=1024,
                     help="output entries compared with the double-double reference (and native matmul)")
@@ -377,7 +379,7 @@ def main() -> int:
         a = workloads.complex_matrix(n, k, sa)
         A = to_dev(a)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.complex128, device=dev))
-        call = lambda N: o2m.zherk_2m(A, n_moduli=N, out=C, scaling=rule)
+        call = lambda N: o2m.zherk_2m(A, n_moduli=N, out=C, scaling=rule, uplo=args.uplo)
         flops, int8_per_n = 4.0 * n * n * k, 2.0 * n * n * k
         metric = "effective ZHERK TFLOP/s (4n^2k/t)"
         desc = f"zherk_2m n={n} k={k} complex128 N(0,1), {{N}} 2M moduli, lower triangle"
@@ -388,7 +390,7 @@ def main() -> int:
         a = workloads.real_matrix(n, k, sa)
         A = to_dev(a)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.float64, device=dev))
-        call = lambda N: o2m.dsyrk_2m(A, n_moduli=N, out=C, scaling=rule)
+        call = lambda N: o2m.dsyrk_2m(A, n_moduli=N, out=C, scaling=rule, uplo=args.uplo)
         flops, int8_per_n = 1.0 * n * n * k, 2.0 * n * n * ((k + 1) // 2)
         metric = "effective DSYRK TFLOP/s (n^2k/t)"
         desc = f"dsyrk_2m n={n} k={k} float64 N(0,1), {{N}} 2M moduli, lower triangle"
@@ -400,7 +402,7 @@ def main() -> int:
         b = workloads.complex_matrix(n, k, sb)
         A, B = to_dev(a), to_dev(b)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.complex128, device=dev))
-        call = lambda N: o2m.zher2k_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        call = lambda N: o2m.zher2k_2m(A, B, n_moduli=N, out=C, scaling=rule, uplo=args.uplo)
         flops, int8_per_n = 8.0 * n * n * k, 4.0 * n * n * k   # N GEMMs n x n x 2k
         metric = "effective ZHER2K TFLOP/s (8n^2k/t)"
         desc = f"zher2k_2m n={n} k={k} complex128 N(0,1), {{N}} 2M moduli, lower triangle"
@@ -412,7 +414,7 @@ def main() -> int:
         b = workloads.real_matrix(n, k, sb)
         A, B = to_dev(a), to_dev(b)
         C = o2m.colmajor(torch.zeros((n, n), dtype=torch.float64, device=dev))
-        call = lambda N: o2m.dsyr2k_2m(A, B, n_moduli=N, out=C, scaling=rule)
+        call = lambda N: o2m.dsyr2k_2m(A, B, n_moduli=N, out=C, scaling=rule, uplo=args.uplo)
         flops, int8_per_n = 2.0 * n * n * k, 4.0 * n * n * ((k + 1) // 2)
         metric = "effective DSYR2K TFLOP/s (2n^2k/t)"
         desc = f"dsyr2k_2m n={n} k={k} float64 N(0,1), {{N}} 2M moduli, lower triangle"
@@ -556,6 +558,7 @@ def main() -> int:
             "config": {"workload": desc.format(N=N), "op": op, "m": m, "n": n, "k": k, "n_moduli": N,
                        "phi": args.phi if op == "zgemm" else None, "scaling_rule": rule,
                        **({} if (ta, tb) == ("N", "N") else {"transa": ta, "transb": tb}),
+                       **({"uplo": args.uplo} if op in ("zherk", "dsyrk", "zher2k", "dsyr2k") else {}),
                        "parallelism": "single GPU"},
             "int8_mfma_util": round(achieved / PEAK_INT8_TOPS, 4),
             "int8_mfma_ceiling": ceiling,

@@ -158,29 +158,34 @@ o2m_status cgemm_2m(int m, int n, int k, const float *A, int lda, const float *B
                     float *C, int ldc, int n_moduli, void *stream);
 
 /* HERK, C = A A^H, A n x k complex128 (Section 5): one int8 GEMM per modulus
-   (C+ = A+ A-^T, C- = C+^T).  uplo must be 'L' or 'l': the lower triangle
-   including the diagonal is written, with Im(c_ii) = 0 exactly; the strictly
-   upper triangle of C is not touched. */
+   (C+ = A+ A-^T, C- = C+^T).  uplo 'L' or 'l': the lower triangle including
+   the diagonal is written, with Im(c_ii) = 0 exactly, and the strictly upper
+   triangle of C is not touched; 'U' or 'u': the upper triangle likewise (the
+   Section 5 text allows either; both are the same exact values, c_ji =
+   conj(c_ij)). */
 o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
                     int n_moduli, void *stream);
 
 /* SYRK, C = A A^T, A n x k real fp64 (Section 5): Z = A[:, :k'] + i A[:, k':]
    with k' = ceil(k/2) (a zero column pads odd k), C = Re(Z Z^H) by the 2M
-   HERK.  uplo 'L' or 'l': lower triangle of the real n x n C written. */
+   HERK.  uplo 'L' or 'l' ('U' or 'u'): lower (upper) triangle of the real
+   n x n C written. */
 o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc,
                     int n_moduli, void *stream);
 
 /* HER2K, C = A B^H + B A^H, A and B n x k complex128 (Section 5).  Row i of
    A and row i of B share one scale (sigma = tau), so the two products add in
    the residue domain: per modulus one int8 GEMM over k' = 2k,
-   C+ = [A+ | B+] [B- | A-]^T, and C- = C+^T.  uplo 'L' or 'l': the lower
-   triangle with Im(c_ii) = 0 exactly is written.  Requires 2k <= 149130. */
+   C+ = [A+ | B+] [B- | A-]^T, and C- = C+^T.  uplo 'L' or 'l' ('U' or 'u'):
+   the lower (upper) triangle with Im(c_ii) = 0 exactly is written.  Requires
+   2k <= 149130. */
 o2m_status zher2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
                      double *C, int ldc, int n_moduli, void *stream);
 
 /* SYR2K, C = A B^T + B A^T, A and B n x k real fp64 (Section 5): the HER2K of
    Z_A = A[:, :k'] + i A[:, k':] and Z_B likewise, k' = ceil(k/2), real part.
-   uplo 'L' or 'l': lower triangle.  Requires 2 ceil(k/2) <= 149130. */
+   uplo 'L' or 'l' ('U' or 'u'): lower (upper) triangle.  Requires
+   2 ceil(k/2) <= 149130. */
 o2m_status dsyr2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb,
                      double *C, int ldc, int n_moduli, void *stream);
 

@@ -207,27 +207,35 @@ def _sym_out(out, n, dtype, device):
     return colmajor(torch.zeros((n, n), dtype=dtype, device=device)) if out is None else out
 
 
+def _uplo(uplo: str) -> bytes:
+    if uplo not in ("L", "U", "l", "u"):
+        raise ValueError(f"uplo must be 'L' or 'U', got {uplo!r}")
+    return uplo.upper().encode()
+
+
 def zherk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None,
-             scaling: str = "max") -> torch.Tensor:
-    """Lower triangle of C = A A^H (complex128 A, n x k).  The strictly upper
-    triangle of a fresh output is zero-initialised; of ``out`` it is left alone."""
+             scaling: str = "max", uplo: str = "L") -> torch.Tensor:
+    """Lower (uplo 'L') or upper ('U') triangle of C = A A^H (complex128 A,
+    n x k).  The other strict triangle of a fresh output is zero-initialised;
+    of ``out`` it is left alone."""
     if A.dtype != torch.complex128 or not A.is_cuda:
         raise TypeError("A must be a complex128 device tensor")
     n, k = A.shape
     out = _sym_out(out, n, torch.complex128, A.device)
-    _check(_L.zherk_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+    _check(_L.zherk_2m_ex(_uplo(uplo), n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
                           _rule(scaling), _stream(stream)), "zherk_2m")
     return out
 
 
 def dsyrk_2m(A: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None, stream=None,
-             scaling: str = "max") -> torch.Tensor:
-    """Lower triangle of C = A A^T (float64 A, n x k) via the half-k 2M HERK."""
+             scaling: str = "max", uplo: str = "L") -> torch.Tensor:
+    """Lower or upper triangle of C = A A^T (float64 A, n x k) via the half-k
+    2M HERK."""
     if A.dtype != torch.float64 or not A.is_cuda:
         raise TypeError("A must be a float64 device tensor")
     n, k = A.shape
     out = _sym_out(out, n, torch.float64, A.device)
-    _check(_L.dsyrk_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
+    _check(_L.dsyrk_2m_ex(_uplo(uplo), n, k, A.data_ptr(), _ld(A), out.data_ptr(), _ld(out), n_moduli,
                           _rule(scaling), _stream(stream)), "dsyrk_2m")
     return out
 
@@ -241,24 +249,24 @@ def _check_pair(A, B, dtype):
 
 
 def zher2k_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
-              stream=None, scaling: str = "max") -> torch.Tensor:
-    """Lower triangle of C = A B^H + B A^H (complex128 A, B: n x k)."""
+              stream=None, scaling: str = "max", uplo: str = "L") -> torch.Tensor:
+    """Lower or upper triangle of C = A B^H + B A^H (complex128 A, B: n x k)."""
     _check_pair(A, B, torch.complex128)
     n, k = A.shape
     out = _sym_out(out, n, torch.complex128, A.device)
-    _check(_L.zher2k_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+    _check(_L.zher2k_2m_ex(_uplo(uplo), n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
                            n_moduli, _rule(scaling), _stream(stream)), "zher2k_2m")
     return out
 
 
 def dsyr2k_2m(A: torch.Tensor, B: torch.Tensor, n_moduli: int = 16, out: torch.Tensor | None = None,
-              stream=None, scaling: str = "max") -> torch.Tensor:
-    """Lower triangle of C = A B^T + B A^T (float64 A, B: n x k) via the
-    half-k 2M HER2K."""
+              stream=None, scaling: str = "max", uplo: str = "L") -> torch.Tensor:
+    """Lower or upper triangle of C = A B^T + B A^T (float64 A, B: n x k) via
+    the half-k 2M HER2K."""
     _check_pair(A, B, torch.float64)
     n, k = A.shape
     out = _sym_out(out, n, torch.float64, A.device)
-    _check(_L.dsyr2k_2m_ex(b"L", n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+    _check(_L.dsyr2k_2m_ex(_uplo(uplo), n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
                            n_moduli, _rule(scaling), _stream(stream)), "dsyr2k_2m")
     return out
 

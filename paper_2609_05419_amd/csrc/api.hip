@@ -279,6 +279,7 @@ struct Call {
     int32_t *E_out, *F_out;
     bool noalloc = false;     // workspace = the static scratch array
     char ta = 'N', tb = 'N';  // GEMM operands: op(X) = X, X^T or X^H ('N', 'T', 'C')
+    bool upper = false;       // symmetric ops: write the upper triangle
 };
 
 bool is_sym(Op op) { return op == kOpH || op == kOpS || op == kOpH2 || op == kOpS2; }
@@ -443,6 +444,7 @@ o2m_status run(const Call &c) {
     ca.amaxB = b.amax_b;
     ca.k = c.k;
     ca.status = status;
+    ca.upper = c.upper;
     for (int l = 0; l < c.N; ++l) {
         ca.hmod[l] = (short)t->res.mod[l];
         ca.hroot[l] = (short)t->res.root[l];
@@ -487,7 +489,7 @@ o2m_status check_gemm(int m, int n, int k, const void *A, int lda, const void *B
 }
 
 o2m_status check_sym(char uplo, int n, int k, const void *A, int lda, const void *C, int ldc, int N) {
-    if (uplo != 'L' && uplo != 'l') return -1;
+    if (uplo != 'L' && uplo != 'l' && uplo != 'U' && uplo != 'u') return -1;
     if (n < 0) return -2;
     if (k < 0) return -3;
     if (!A && n > 0 && k > 0) return -4;
@@ -502,7 +504,7 @@ o2m_status check_sym(char uplo, int n, int k, const void *A, int lda, const void
 // rank-2k: the GEMMs run over [A | B], so twice the (SYRK-split) k must fit
 o2m_status check_sym2(char uplo, int n, int k, const void *A, int lda, const void *B, int ldb, const void *C,
                       int ldc, int N, bool split) {
-    if (uplo != 'L' && uplo != 'l') return -1;
+    if (uplo != 'L' && uplo != 'l' && uplo != 'U' && uplo != 'u') return -1;
     if (n < 0) return -2;
     if (k < 0) return -3;
     if (!A && n > 0 && k > 0) return -4;
@@ -632,8 +634,10 @@ o2m_status zherk_2m_ex(char uplo, int n, int k, const double *A, int lda, double
     o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpH, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
-                    nullptr, nullptr});
+    Call c{kOpH, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr};
+    c.upper = uplo == 'U' || uplo == 'u';
+    return run(c);
 }
 
 o2m_status zherk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
@@ -646,8 +650,10 @@ o2m_status dsyrk_2m_ex(char uplo, int n, int k, const double *A, int lda, double
     o2m_status s = check_sym(uplo, n, k, A, lda, C, ldc, n_moduli);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpS, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
-                    nullptr, nullptr});
+    Call c{kOpS, n, n, k, A, lda, nullptr, 1, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr};
+    c.upper = uplo == 'U' || uplo == 'u';
+    return run(c);
 }
 
 o2m_status dsyrk_2m(char uplo, int n, int k, const double *A, int lda, double *C, int ldc, int n_moduli,
@@ -660,8 +666,10 @@ o2m_status zher2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const
     o2m_status s = check_sym2(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, false);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpH2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
-                    nullptr, nullptr});
+    Call c{kOpH2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr};
+    c.upper = uplo == 'U' || uplo == 'u';
+    return run(c);
 }
 
 o2m_status zher2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,
@@ -674,8 +682,10 @@ o2m_status dsyr2k_2m_ex(char uplo, int n, int k, const double *A, int lda, const
     o2m_status s = check_sym2(uplo, n, k, A, lda, B, ldb, C, ldc, n_moduli, true);
     if (s == O2M_OK) s = check_scaling(scaling);
     if (s != O2M_OK || n == 0) return s;
-    return run(Call{kOpS2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
-                    nullptr, nullptr});
+    Call c{kOpS2, n, n, k, A, lda, B, ldb, C, ldc, n_moduli, scaling, (hipStream_t)stream, nullptr,
+                    nullptr, nullptr};
+    c.upper = uplo == 'U' || uplo == 'u';
+    return run(c);
 }
 
 o2m_status dsyr2k_2m(char uplo, int n, int k, const double *A, int lda, const double *B, int ldb, double *C,

@@ -219,7 +219,10 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     __shared__ __attribute__((aligned(16))) int8_t tl[2][2][32 * 32];
     const SymTile st = sym_tile_of(blockIdx.x, (a.n + 31) / 32);
     if (!st.valid) return;  // idle slot or strictly upper tile: nothing to write
-    const int I = st.I, J = st.J;
+    // tile (I, J) of the lower triangle, or its mirror (J, I) for the upper:
+    // entry (i, j) needs C+ at (i, j) and (j, i) either way, and the same
+    // coalesced layout writes it
+    const int I = a.upper ? st.J : st.I, J = a.upper ? st.I : st.J;
     const int tid = threadIdx.x;
     // the thread's entries: rows r0 + 8e (e = 0..3) of column jl, so that each
     // store writes whole 128-byte lines across 8 lanes
@@ -267,7 +270,7 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int i = I * 32 + r0 + 8 * e;
-        if (i >= a.n || j >= a.n || i < j) continue;
+        if (i >= a.n || j >= a.n || (a.upper ? i > j : i < j)) continue;
         const int ei = a.E[i], ej = a.E[j];
         const bool bad = ei == INT32_MIN || ej == INT32_MIN;
         const int sc = ei + ej + a.scale_bias;

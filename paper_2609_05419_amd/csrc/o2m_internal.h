@@ -236,6 +236,7 @@ struct CrtArgs {
     const unsigned long long *amaxA, *amaxB;  // gauss mode bound check
     int k;
     int *status;
+    int upper;          // HERK/SYRK/rank-2k: write the upper triangle instead of the lower
     short hmod[kMaxModuli], hroot[kMaxModuli];  // hook mode: moduli and roots
 };
 // Both go to the CRT kernels by value: stay within the kernel-argument limit.

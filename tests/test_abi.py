@@ -109,7 +109,7 @@ def test_argument_errors_are_reported_before_any_gpu_work(lib):
     lib.gauss_gemm_2m.argtypes = lib.zgemm_2m.argtypes
     assert lib.gauss_gemm_2m(4, 4, 4, fake, 4, fake, 4, fake, 4, 9, None) == -20
     lib.zherk_2m.argtypes = [ctypes.c_char, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int, P]
-    assert lib.zherk_2m(b"U", 4, 4, fake, 4, fake, 4, 16, None) == -1
+    assert lib.zherk_2m(b"X", 4, 4, fake, 4, fake, 4, 16, None) == -1
     assert lib.zherk_2m(b"L", 4, 4, fake, 4, fake, 4, 23, None) == -20    # symmetric calls: 2M only
     assert lib.zherk_2m(b"L", 4, 4, fake, 3, fake, 4, 16, None) == -5
     assert lib.zherk_2m(b"L", 0, 4, None, 1, None, 1, 16, None) == 0
@@ -155,7 +155,7 @@ def test_rank2k_and_scaling_argument_errors(lib):
     fake = P(0x1000)
     lib.zher2k_2m.argtypes = [C, I, I, P, I, P, I, P, I, I, P]
     f = lib.zher2k_2m
-    assert f(b"U", 4, 4, fake, 4, fake, 4, fake, 4, 16, None) == -1
+    assert f(b"X", 4, 4, fake, 4, fake, 4, fake, 4, 16, None) == -1
     assert f(b"L", -1, 4, fake, 4, fake, 4, fake, 4, 16, None) == -2
     assert f(b"L", 4, -1, fake, 4, fake, 4, fake, 4, 16, None) == -3
     assert f(b"L", 4, 4, None, 4, fake, 4, fake, 4, 16, None) == -4

@@ -372,3 +372,43 @@ def test_cs_k_at_the_int32_limit_sampled(o2m):
     ok = same_bits(got, O.oq_zgemm(a, b, N, entries=ent, scaling="cs"))
     report("cs k=149130", bitexact=ok)
     assert ok
+
+
+# ------------------------------------------------------------ upper triangles
+# uplo 'U': the symmetric calls write the upper triangle (the mirrored tile
+# pairs of the CRT kernel), leave the strictly lower one untouched, and give
+# the same exact values as the lower triangle (c_ji = conj(c_ij)).
+
+UP = lambda n: np.triu(np.ones((n, n), dtype=bool))
+
+
+@pytest.mark.parametrize("rule", ["max", "cs"])
+@pytest.mark.parametrize("n,k", [(77, 130), (300, 65)])
+def test_symmetric_calls_upper_triangle(o2m, n, k, rule):
+    N = 16
+    a = W.complex_matrix(n, k, 5301 + n, dist="phi", phi=2.0)
+    b = W.complex_matrix(n, k, 5302 + n, dist="phi", phi=2.0)
+    r, s = W.real_matrix(n, k, 5303 + n, dist="phi", phi=2.0), W.real_matrix(n, k, 5304 + n)
+    up, low = UP(n), ~UP(n)
+    zc = 7.5 - 2.5j
+
+    def check(name, call, ref, sentinel, dtype):
+        C = o2m.colmajor(torch.full((n, n), sentinel, dtype=dtype, device=DEV))
+        call(C, "U")
+        got = host(C)
+        ok = same_bits(got[up], ref[up]) and bool((got[low] == sentinel).all())
+        lower = host(call(o2m.colmajor(torch.zeros((n, n), dtype=dtype, device=DEV)), "L"))
+        mirror = np.array_equal(np.conj(lower.T)[up], got[up])      # values: -0 and +0 compare equal
+        report("upper", op=name, n=n, k=k, rule=rule, bitexact=ok, mirror=mirror)
+        assert ok and mirror
+        if np.iscomplexobj(got):
+            assert (np.diag(got).imag == 0).all()
+
+    check("zherk", lambda C, u: o2m.zherk_2m(to_dev(a), n_moduli=N, out=C, scaling=rule, uplo=u),
+          O.oq_zherk(a, N, scaling=rule), zc, torch.complex128)
+    check("zher2k", lambda C, u: o2m.zher2k_2m(to_dev(a), to_dev(b), n_moduli=N, out=C, scaling=rule, uplo=u),
+          O.oq_zher2k(a, b, N, scaling=rule), zc, torch.complex128)
+    check("dsyrk", lambda C, u: o2m.dsyrk_2m(to_dev(r), n_moduli=N, out=C, scaling=rule, uplo=u),
+          O.oq_dsyrk(r, N, scaling=rule), -3.25, torch.float64)
+    check("dsyr2k", lambda C, u: o2m.dsyr2k_2m(to_dev(r), to_dev(s), n_moduli=N, out=C, scaling=rule, uplo=u),
+          O.oq_dsyr2k(r, s, N, scaling=rule), -3.25, torch.float64)
