@@ -169,11 +169,16 @@ def test_randomized_configurations(o2m):
     O2M_RANDOM_SEED widen the sweep (default: 36 cases, seed 2609);
     O2M_RANDOM_TALL=1 draws m up to 1300 (several 256-row waves of the CRT's
     row-order stores, several 128 x 128 super-tiles of the symmetric CRT) with
-    n and k up to 200 instead of all three up to 300."""
-    rng = np.random.default_rng(int(os.environ.get("O2M_RANDOM_SEED", "2609")))
+    n and k up to 200 instead of all three up to 300.  A second generator
+    draws the operand layout (op(A), op(B) of the GEMMs, the triangle of the
+    symmetric calls), so the first one's cases stay those of earlier sweeps."""
+    seed0 = int(os.environ.get("O2M_RANDOM_SEED", "2609"))
+    rng = np.random.default_rng(seed0)
+    lay = np.random.default_rng(seed0 + 1)
     tall = os.environ.get("O2M_RANDOM_TALL") == "1"
     ops = ["zgemm", "cgemm", "zherk", "dsyrk", "zher2k", "dsyr2k"]
-    low = lambda n: np.tril(np.ones((n, n), dtype=bool))
+    tri = lambda n, u: np.triu(np.ones((n, n), dtype=bool)) if u == "U" else np.tril(np.ones((n, n), dtype=bool))
+    stored = lambda x, t: x if t == "N" else (x.T if t == "T" else x.conj().T)
     for case in range(int(os.environ.get("O2M_RANDOM_CASES", "36"))):
         op = ops[case % len(ops)]
         sym = op not in ("zgemm", "cgemm")
@@ -190,30 +195,37 @@ def test_randomized_configurations(o2m):
         dist = ["normal", "uniform", "phi"][int(rng.integers(0, 3))]
         phi = float(rng.choice([0.5, 2.0, 4.0]))
         seed = 9000 + case
-        print(f"[hybrid] random case {case}: {op} m={m} n={n} k={k} N={N} {rule} {dist}", flush=True)
+        ta, tb = (str(x) for x in lay.choice(list("NTC"), 2))
+        up = str(lay.choice(["L", "U"]))
+        print(f"[hybrid] random case {case}: {op} m={m} n={n} k={k} N={N} {rule} {dist} "
+              + (f"op={ta}{tb}" if not sym else f"uplo={up}"), flush=True)
         if op in ("zgemm", "cgemm"):
             dt = np.complex128 if op == "zgemm" else np.complex64
             a = W.complex_matrix(m, k, seed, dist=dist, phi=phi, dtype=dt)
             b = W.complex_matrix(k, n, seed + 1, dist=dist, phi=phi, dtype=dt)
-            fn = o2m.zgemm_2m if op == "zgemm" else o2m.cgemm_2m
+            fn = o2m.zgemm_2m_op if op == "zgemm" else o2m.cgemm_2m_op
             ofn = O.oq_zgemm if op == "zgemm" else O.oq_cgemm
-            got = host(fn(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+            A = to_dev(np.ascontiguousarray(stored(a, ta)))
+            B = to_dev(np.ascontiguousarray(stored(b, tb)))
+            got = host(fn(A, B, ta, tb, n_moduli=N, scaling=rule))
             assert same_bits(got, ofn(a, b, N, scaling=rule)), case
         elif op in ("zherk", "zher2k"):
             a = W.complex_matrix(m, k, seed, dist=dist, phi=phi)
             if op == "zherk":
-                got, ref = host(o2m.zherk_2m(to_dev(a), n_moduli=N, scaling=rule)), O.oq_zherk(a, N, scaling=rule)
+                got = host(o2m.zherk_2m(to_dev(a), n_moduli=N, scaling=rule, uplo=up))
+                ref = O.oq_zherk(a, N, scaling=rule)
             else:
                 b = W.complex_matrix(m, k, seed + 1, dist=dist, phi=phi)
-                got = host(o2m.zher2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+                got = host(o2m.zher2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule, uplo=up))
                 ref = O.oq_zher2k(a, b, N, scaling=rule)
-            assert same_bits(got[low(m)], ref[low(m)]), case
+            assert same_bits(got[tri(m, up)], ref[tri(m, up)]), case
         else:
             a = W.real_matrix(m, k, seed, dist=dist, phi=phi)
             if op == "dsyrk":
-                got, ref = host(o2m.dsyrk_2m(to_dev(a), n_moduli=N, scaling=rule)), O.oq_dsyrk(a, N, scaling=rule)
+                got = host(o2m.dsyrk_2m(to_dev(a), n_moduli=N, scaling=rule, uplo=up))
+                ref = O.oq_dsyrk(a, N, scaling=rule)
             else:
                 b = W.real_matrix(m, k, seed + 1, dist=dist, phi=phi)
-                got = host(o2m.dsyr2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule))
+                got = host(o2m.dsyr2k_2m(to_dev(a), to_dev(b), n_moduli=N, scaling=rule, uplo=up))
                 ref = O.oq_dsyr2k(a, b, N, scaling=rule)
-            assert same_bits(got[low(m)], ref[low(m)]), case
+            assert same_bits(got[tri(m, up)], ref[tri(m, up)]), case
