@@ -8,11 +8,13 @@
 // column-major), shared with the three neighbouring tiles of the same column
 // strip, and each XCD fetches into its own L2.  Dispatched in index order the
 // four tiles that share a line run on four XCDs, and the line crosses the
-// fabric four times.  Instead, super-tiles of 4 x 4 tiles (128 x 128, the
+// fabric four times.  Instead, super-tiles of 16 x 16 tiles (512 x 512, the
 // lower triangle in row-major order) are dealt round-robin to the XCDs, and
-// the 16 workgroups of one super-tile take 16 consecutive slots of the same
-// XCD, so that a line is fetched once and serves all four tiles from L2.
-// Tiles above the diagonal (in diagonal super-tiles) and beyond nb idle.
+// the 256 workgroups of one super-tile take 256 consecutive slots of the same
+// XCD (about as many as it holds at once), so that a line is fetched once and
+// serves all four tiles from L2, and the workgroups of a super-tile read each
+// column of the plane in 512-byte runs.  Tiles above the diagonal (in
+// diagonal super-tiles) and beyond nb idle.
 #pragma once
 
 #include <cmath>
@@ -24,7 +26,7 @@
 namespace o2m {
 
 constexpr int kSymXcds = 8;   // workgroup b is dispatched to XCD b % 8
-constexpr int kSymSuper = 4;  // tiles per super-tile side
+constexpr int kSymSuper = 16;  // tiles per super-tile side
 
 struct SymTile {
     int I, J;  // tile-row and tile-column of the output tile

@@ -160,8 +160,9 @@ SYM_NB = [0, 1, 2, 3, 4, 5, 7, 8, 9, 31, 32, 33, 63, 64, 65, 127, 255, 256, 257,
 @pytest.mark.parametrize("nb", SYM_NB)
 def test_sym_tiles_cover_lower_triangle_once(lib, nb):
     grid = lib.t_sym_grid(nb)
-    ns = -(-nb // 4)
-    assert grid == 8 * 16 * -(-(ns * (ns + 1) // 2) // 8)
+    S = 16  # tiles per super-tile side
+    ns = -(-nb // S)
+    assert grid == 8 * S * S * -(-(ns * (ns + 1) // 2) // 8)
     t = np.zeros((max(grid, 1), 3), dtype=np.int32)
     lib.t_sym_tiles(nb, grid, t.ctypes.data)
     t = t[:grid]
@@ -171,25 +172,25 @@ def test_sym_tiles_cover_lower_triangle_once(lib, nb):
     assert (I < nb).all() and (J >= 0).all() and (I >= J).all()
     assert len(set(zip(I.tolist(), J.tolist()))) == len(I)
     # the tiles sharing a line: same J, I // 4 (own tile) and same I, J // 4
-    # (mirrored tile) -- all in one super-tile on one XCD, in 16 consecutive slots
+    # (mirrored tile) -- all in one super-tile on one XCD, in S * S consecutive slots
     b = np.nonzero(v)[0]
-    key = (I // 4) * (ns + 1) + J // 4
+    key = (I // S) * (ns + 1) + J // S
     for k in np.unique(key):
         members = b[key == k]
         assert len(set((members % 8).tolist())) == 1
         slots = members // 8
-        assert slots.max() - slots.min() < 16 and len(set((slots // 16).tolist())) == 1
+        assert slots.max() - slots.min() < S * S and len(set((slots // (S * S)).tolist())) == 1
 
 
 def test_sym_tile_of_large_grids(lib):
     # super-tile rows near triangular numbers, where a float square root could round
     # the row index the wrong way
-    nb = 1 << 22
+    nb = 1 << 24
     out = np.zeros(3, dtype=np.int32)
     for k in (1, 2, 3, 1000, 46340, 46341, 1 << 19, (1 << 20) - 1):
         for s in (k * (k + 1) // 2 - 1, k * (k + 1) // 2, k * (k + 1) // 2 + 1):
-            b = (s // 8) * 128 + s % 8  # the first workgroup (sub-tile 0) of super-tile s
+            b = (s // 8) * 8 * 256 + s % 8  # the first workgroup (sub-tile 0) of super-tile s
             lib.t_sym_tile_of(b, nb, out.ctypes.data)
             si = (math.isqrt(8 * s + 1) - 1) // 2  # exact integer square root
-            assert (out[1], out[2]) == (4 * si, 4 * (s - si * (si + 1) // 2)), (k, s)
+            assert (out[1], out[2]) == (16 * si, 16 * (s - si * (si + 1) // 2)), (k, s)
             assert out[0] == 1
