@@ -53,6 +53,36 @@ O2M_HD inline double sum3_rn(double a, double b, double c) {
     return th + sum_round_odd(tl, ul);
 }
 
+// RN(c2 2^80 + c1 2^40 + c0) for integer-valued limbs with |c_t| < 2^52.4
+// (the lifted limbs of a three-limb CRT value: limb sums below 2^52 minus
+// q M_t with |q| < 2^11.4 and |M_t| <= 2^39).  Carrying the two low limbs
+// into balanced digits, c = A + B + d0 with A = c2' 2^80, B = d1 2^40 and
+// |d1|, |d0| <= 2^39, every step exact.  s = RN(A + B) has the exact error
+// e = A + B - s (fast two-sum: |A| >= 2^80 > |B| unless A = 0, when e = 0),
+// a multiple of 2^40.  If e = 0, RN(c) = RN(s + d0).  Otherwise the doubles
+// next to s are at least 2^41 away and |d0| <= 2^39 is at most a quarter of
+// that, so c rounds to s unless A + B was exactly halfway (|e| half the gap
+// on e's side) and d0 pushes c past that midpoint (e d0 > 0): then RN(c) is
+// the neighbour s + 2e.  |e| is half the gap exactly when s + 2e is a double
+// (otherwise it lies strictly between s and the neighbour), which
+// RN(s + 2e) - s == 2e tests.  And when RN(c) = s, RN(s + d0) = s too (d0
+// never reaches half a gap, and a tie at exactly 2^39 below a power of two
+// goes to s, whose significand is even).
+O2M_HD inline double round3_rn(double c0, double c1, double c2) {
+    const double h0 = rint(c0 * 0x1p-40);
+    const double d0 = fma(-h0, kTwo40, c0);
+    c1 += h0;
+    const double h1 = rint(c1 * 0x1p-40);
+    const double d1 = fma(-h1, kTwo40, c1);
+    c2 += h1;
+    const double A = c2 * kTwo80;
+    const double s = fma(d1, kTwo40, A);
+    const double e = fma(d1, kTwo40, -(s - A));
+    const double n = fma(2.0, e, s);
+    const bool past_tie = n - s == 2.0 * e && e * d0 > 0.0;
+    return past_tie ? n : s + d0;
+}
+
 // Two's complement integer of W 64-bit words, little-endian.
 template <int W>
 struct UW {
@@ -252,8 +282,9 @@ O2M_HD inline void top3_of(double (&c)[T], double &a, double &b, double &low) {
 }
 
 // Steps 5-7 for one component with fp64 output: the lifted limbs, then
-// RN(c 2^sc), one rounding.  c is rounded with the exact limb sum (T = 2) or
-// the three-term sum (T = 3; T >= 4 through top3_of) and scaled by 2^sc,
+// RN(c 2^sc), one rounding.  c is rounded with the exact limb sum (T = 2),
+// round3_rn (T = 3) or the three-term sum (T >= 4, through top3_of) and
+// scaled by 2^sc,
 // which is exact unless the result is subnormal; such results (and those that
 // underflow to zero) are rounded again from the exact integer, held as 192 or
 // 256 bits, at the subnormal quantum.
@@ -265,7 +296,7 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     if constexpr (T == 2) {
         x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
     } else if constexpr (T == 3) {
-        x = sum3_rn(c[2] * kTwo80, c[1] * kTwo40, c[0]);
+        x = round3_rn(c[0], c[1], c[2]);
     } else {
         double a, b, low;
         top3_of<T>(c, a, b, low);

@@ -20,6 +20,7 @@ double round_fmt(const int64_t *limbs, int T, int sc, int f32) {
 
 extern "C" {
 double t_sum3_rn(double a, double b, double c) { return o2m::sum3_rn(a, b, c); }
+double t_round3_rn(double c0, double c1, double c2) { return o2m::round3_rn(c0, c1, c2); }
 double t_sum3_ro(double a, double b, double c) { return o2m::sum3_ro(a, b, c); }
 double t_sum_ro(double a, double b) { return o2m::sum_round_odd(a, b); }
 // T limbs (T <= 6) rounded into fp64 (f32 = 0) or fp32 (f32 = 1) after 2^sc

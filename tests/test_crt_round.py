@@ -26,6 +26,8 @@ def lib(tmp_path_factory):
     D, P, I = ctypes.c_double, ctypes.c_void_p, ctypes.c_int
     L.t_sum3_rn.argtypes = [D, D, D]
     L.t_sum3_rn.restype = D
+    L.t_round3_rn.argtypes = [D, D, D]
+    L.t_round3_rn.restype = D
     L.t_round_limbs.argtypes = [P, I, I]
     L.t_round_limbs.restype = D
     L.t_lift_round.argtypes = [P, I, P, D, I, I]
@@ -102,6 +104,72 @@ def test_three_term_sum_is_correctly_rounded(lib):
         c0, c1, c2 = split_limbs(c, 3, rng)
         got = lib.t_sum3_rn(float(c2) * 2.0 ** 80, float(c1) * 2.0 ** 40, float(c0))
         assert got == float(c), c
+
+
+def three_limb_cases(rng):
+    """Integers below 2^119 that stress the three-limb rounding: the generic
+    mix above, exact midpoints of the 53-bit grid that are multiples of 2^40
+    (where the high part alone ties) moved by a low digit in [-2^39, 2^39],
+    and values around powers of two, where the gaps on the two sides differ."""
+    vals = interesting_integers(rng, 119)
+    for _ in range(4000):
+        s = rng.randint(41, 119 - 53)
+        m = rng.randint(1 << 52, (1 << 53) - 1)
+        mid = (m << s) + (1 << (s - 1))
+        d = rng.choice((0, 1, -1, 1 << 39, -(1 << 39), rng.randint(-(1 << 39), 1 << 39)))
+        v = mid + d
+        vals.append(v if rng.random() < 0.5 else -v)
+    for k in range(41, 119):
+        p = 1 << k
+        for d in (0, 1, -1, 1 << 39, -(1 << 39), p >> 53, -(p >> 54), (p >> 53) + 1, -(p >> 54) - 1,
+                  -(p >> 54) + 1, (p >> 53) - 1):
+            for v in (p + d, p - (p >> 54) + d):
+                vals.append(v if rng.random() < 0.5 else -v)
+    return vals
+
+
+def test_three_limb_rounding(lib):
+    """round3_rn (the lift's rounding for three limbs) equals Python's
+    correctly rounded int -> float on every case, for limbs split at random
+    (carries of up to 2^11 between limbs, as the lift leaves them)."""
+    rng = random.Random(5)
+    for c in three_limb_cases(rng):
+        for _ in range(2):
+            c0, c1, c2 = split_limbs(c, 3, rng)
+            got = lib.t_round3_rn(float(c0), float(c1), float(c2))
+            assert got == float(c), (c, c0, c1, c2)
+            assert np.float64(got).view(np.uint64) == np.float64(float(c)).view(np.uint64)
+
+
+def test_three_limb_rounding_catches_a_dropped_tie_step():
+    """The cases above hold inputs on which skipping the past-the-midpoint
+    step (returning RN(s + d0) always) or the low-digit carry gives a wrong
+    result, so the test would catch either mistake."""
+    rng = random.Random(5)
+
+    def model(c0, c1, c2, tie_step=True, carry=True):
+        # the same steps on Python integers, each rounding to a double explicit
+        h0 = round(c0 / 2 ** 40) if carry else 0
+        d0 = c0 - h0 * 2 ** 40
+        c1 = c1 + h0
+        h1 = round(c1 / 2 ** 40)
+        d1 = c1 - h1 * 2 ** 40
+        c2 = c2 + h1
+        A, B = c2 << 80, d1 << 40
+        s = int(float(A + B))
+        e = A + B - s
+        n = int(float(s + 2 * e))
+        if tie_step and n - s == 2 * e and e * d0 > 0:
+            return float(n)
+        return float(s + d0)
+
+    wrong_tie = wrong_carry = 0
+    for c in three_limb_cases(rng)[:20000]:
+        c0, c1, c2 = split_limbs(c, 3, rng)
+        assert model(c0, c1, c2) == float(c)
+        wrong_tie += model(c0, c1, c2, tie_step=False) != float(c)
+        wrong_carry += model(c0, c1, c2, carry=False) != float(c)
+    assert wrong_tie > 0 and wrong_carry > 0
 
 
 def test_three_term_sum_rounds_to_odd(lib):
