@@ -53,21 +53,40 @@ O2M_HD inline double sum3_rn(double a, double b, double c) {
     return th + sum_round_odd(tl, ul);
 }
 
+// RN(a + b + y) for three terms split on a base-2^40 digit boundary: a and
+// b integer multiples of 2^G (G = 40 (j - 1)), a = 0 or |a| >= 2^(G + 40) >
+// 2^(G + 39) >= |b|, and y = 0 or 0 < |y| < 2^G, given as y itself when a
+// double holds it (always when a = 0) or else rounded to odd.  s = RN(a + b)
+// has the exact error e = (a + b) - s (fast two-sum: |a| >= |b|, or a = 0
+// and e = 0), a multiple of 2^G.  If e = 0, a + b + y rounds like s + y:
+// with a != 0, |s| >= 2^(G + 39), so the doubles and midpoints near s + y
+// are multiples of 2^(G - 15), doubles of y's scale (|y| < 2^G) with an
+// even last bit, which y rounded to odd is not, and it lies on the same
+// side of each of them as y.
+// If e != 0, a + b was not a double, so the doubles next to s are at least
+// 2^(G + 1) apart and |e| + |y| stays below half a gap unless a + b was
+// exactly halfway (|e| half the gap on e's side): then y decides, and the
+// result is the neighbour s + 2e when y points past the midpoint (e y > 0),
+// else s.  |e| is half the gap exactly when s + 2e is a double, i.e. when
+// RN(s + 2e) - s == 2e (otherwise s + 2e lies strictly between s and the
+// neighbour).
+O2M_HD inline double round_top3(double a, double b, double y) {
+    const double s = a + b;
+    const double e = b - (s - a);
+    const double n = fma(2.0, e, s);
+    if (n - s == 2.0 * e && e * y > 0.0) return n;
+    return e == 0.0 ? s + y : s;
+}
+
 // RN(c2 2^80 + c1 2^40 + c0) for integer-valued limbs with |c_t| < 2^52.4
 // (the lifted limbs of a three-limb CRT value: limb sums below 2^52 minus
-// q M_t with |q| < 2^11.4 and |M_t| <= 2^39).  Carrying the two low limbs
-// into balanced digits, c = A + B + d0 with A = c2' 2^80, B = d1 2^40 and
-// |d1|, |d0| <= 2^39, every step exact.  s = RN(A + B) has the exact error
-// e = A + B - s (fast two-sum: |A| >= 2^80 > |B| unless A = 0, when e = 0),
-// a multiple of 2^40.  If e = 0, RN(c) = RN(s + d0).  Otherwise the doubles
-// next to s are at least 2^41 away and |d0| <= 2^39 is at most a quarter of
-// that, so c rounds to s unless A + B was exactly halfway (|e| half the gap
-// on e's side) and d0 pushes c past that midpoint (e d0 > 0): then RN(c) is
-// the neighbour s + 2e.  |e| is half the gap exactly when s + 2e is a double
-// (otherwise it lies strictly between s and the neighbour), which
-// RN(s + 2e) - s == 2e tests.  And when RN(c) = s, RN(s + d0) = s too (d0
-// never reaches half a gap, and a tie at exactly 2^39 below a power of two
-// goes to s, whose significand is even).
+// q M_t with |q| < 2^11.4 and |M_t| <= 2^39).  The two low limbs are carried
+// into balanced digits d1, d0 (|d| <= 2^39, every step exact), and
+// c = c2' 2^80 + d1 2^40 + d0 is rounded as in round_top3 (G = 40, y = d0),
+// except that s + d0 needs no guard for e != 0: then the gaps next to s are
+// at least 2^41 on e's side and 2^40 on the other, so s + d0 rounds to s
+// (at |d0| = 2^39 below a power of two, a tie that goes to s, whose
+// significand is even).
 O2M_HD inline double round3_rn(double c0, double c1, double c2) {
     const double h0 = rint(c0 * 0x1p-40);
     const double d0 = fma(-h0, kTwo40, c0);
@@ -75,12 +94,11 @@ O2M_HD inline double round3_rn(double c0, double c1, double c2) {
     const double h1 = rint(c1 * 0x1p-40);
     const double d1 = fma(-h1, kTwo40, c1);
     c2 += h1;
-    const double A = c2 * kTwo80;
-    const double s = fma(d1, kTwo40, A);
-    const double e = fma(d1, kTwo40, -(s - A));
+    const double a = c2 * kTwo80;
+    const double s = fma(d1, kTwo40, a);
+    const double e = fma(d1, kTwo40, -(s - a));
     const double n = fma(2.0, e, s);
-    const bool past_tie = n - s == 2.0 * e && e * d0 > 0.0;
-    return past_tie ? n : s + d0;
+    return n - s == 2.0 * e && e * d0 > 0.0 ? n : s + d0;
 }
 
 // Two's complement integer of W 64-bit words, little-endian.
@@ -283,8 +301,8 @@ O2M_HD inline void top3_of(double (&c)[T], double &a, double &b, double &low) {
 
 // Steps 5-7 for one component with fp64 output: the lifted limbs, then
 // RN(c 2^sc), one rounding.  c is rounded with the exact limb sum (T = 2),
-// round3_rn (T = 3) or the three-term sum (T >= 4, through top3_of) and
-// scaled by 2^sc,
+// round3_rn (T = 3) or round_top3 of top3_of's terms (T >= 4) and scaled by
+// 2^sc,
 // which is exact unless the result is subnormal; such results (and those that
 // underflow to zero) are rounded again from the exact integer, held as 192 or
 // 256 bits, at the subnormal quantum.
@@ -300,7 +318,7 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     } else {
         double a, b, low;
         top3_of<T>(c, a, b, low);
-        x = sum3_rn(a, b, low);
+        x = round_top3(a, b, low);
     }
     const double r = ldexp(x, sc);
     if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
