@@ -91,10 +91,20 @@ __device__ inline uint32_t pack4(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t
 template <int D> constexpr int per_thread() { return D >= 4 ? 8 : 16; }
 
 // PT residue bytes of one lane, contiguous in the plane (16- or 8-byte store).
+// The stores are non-temporal (no cache allocation): the planes are far
+// larger than the caches and are read back only by the GEMM, from its own
+// tile windows; plain stores measured 4-5% slower for the whole pass.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 template <int PT>
 __device__ inline void store_words(int8_t *dst, const uint32_t (&w)[PT / 4]) {
-    if constexpr (PT == 16) *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
-    else *reinterpret_cast<uint2 *>(dst) = make_uint2(w[0], w[1]);
+    if constexpr (PT == 16) {
+        const u32x4 v = {w[0], w[1], w[2], w[3]};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dst));
+    } else {
+        const u32x2 v = {w[0], w[1]};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst));
+    }
 }
 
 // MODE 0: rows of X (A, column-major m x k): entry (r, kk) at X[r + kk*ld]
