@@ -931,6 +931,27 @@ def test_zgemm_op_matches_plain_call_and_hybrid(o2m):
     assert z.shape == (m, n) and (host(z) == 0).all()
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("rule", ["max", "cs"])
+@pytest.mark.parametrize("ta,tb", [("C", "T"), ("T", "N")])
+def test_zgemm_op_4096_sampled(o2m, ta, tb, rule):
+    """Transposed and conjugated operands of 256 MiB each, large enough for the
+    scaling pass's streaming loads in both scan layouts: sampled entries
+    bit-exact against the oracle on the explicitly formed op(A), op(B)."""
+    m = n = k = 4096
+    N = 16
+    opa = W.complex_matrix(m, k, 4711, dist="phi", phi=0.5)
+    opb = W.complex_matrix(k, n, 4712, dist="phi", phi=0.5)
+    A = to_dev(np.ascontiguousarray(_stored(opa, ta)))
+    B = to_dev(np.ascontiguousarray(_stored(opb, tb)))
+    C = host(o2m.zgemm_2m_op(A, B, ta, tb, n_moduli=N, scaling=rule))
+    ent = _sample(np.random.default_rng(47), m, n, 48)
+    got = np.array([C[i, j] for i, j in ent])
+    ok = same_bits(got, O.oq_zgemm(opa, opb, N, entries=ent, scaling=rule))
+    report("zgemm op 4096^3 sampled", ops=ta + tb, rule=rule, bitexact=ok)
+    assert ok
+
+
 def test_cs_resummed_entries_transposed_operands(o2m):
     """Rows of op(A) read as columns of the stored A, columns of op(B) read as
     rows of the stored B, among them ones whose chunk records leave the
