@@ -13,10 +13,10 @@
 // |c| / M <= 1/2 - 2^-32, far from the rounding boundary, so q is exact.  The
 // lifted value c = X - q M (step 6) is then exact as limbs c_t = S_t - q M_t,
 // and step 7 rounds c 2^(E_i + F_j - pA - pB) once, to nearest with ties to
-// even, into the output type (fp64: the limbs carried into balanced digits
-// and rounded once from the top two plus the sign of the rest, subnormal
-// results from the exact multiword integer; fp32: the limb sum rounded to
-// odd in fp64, then to fp32: crt_round.h).
+// even, into the output type (fp64: the limbs carried into balanced digits,
+// the top two added once with an exact check of the tie against the rest,
+// subnormal results from the exact multiword integer; fp32: the limb sum
+// rounded to odd in fp64, then to fp32: crt_round.h).
 //
 // Hybrid sets (Section 3.2): for the 3M moduli the GEMM left T1 = Ar Br,
 // T2 = Ai Bi, T3 = (Ar + Ai)(Br + Bi) mod m, so u = T1 - T2 and
