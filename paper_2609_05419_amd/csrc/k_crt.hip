@@ -212,11 +212,17 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
 
 // HERK / SYRK: plane l holds C+ = A+ A-^T; C- = C+^T (Section 5), so the
 // entry (i, j) needs C+ at (i, j) and at (j, i).  A workgroup owns a 32 x 32
-// tile of the lower triangle and stages both tiles of every plane in LDS.
+// tile of the lower triangle and stages both tiles of CH planes at a time in
+// LDS; the next CH planes' copies are in flight while these planes' limb sums
+// run.  The real-only form, light on arithmetic, waits on memory and takes 8
+// planes per chunk; the complex form issues twice the limb sums and takes 4,
+// whose staging registers cost less occupancy (measured: 8 planes or copies
+// straight into LDS were slower for it).
 template <int T, bool REAL_ONLY>
 __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
-    // [buffer][P = C+ tile (I, J), Q = C+ tile (J, I)], column-major 32 x 32
-    __shared__ __attribute__((aligned(16))) int8_t tl[2][2][32 * 32];
+    constexpr int CH = REAL_ONLY ? 8 : 4;  // planes per chunk
+    // [plane of the chunk][P = C+ tile (I, J), Q = C+ tile (J, I)], column-major 32 x 32
+    __shared__ __attribute__((aligned(16))) int8_t tl[CH][2][32 * 32];
     const SymTile st = sym_tile_of(blockIdx.x, (a.n + 31) / 32);
     if (!st.valid) return;  // idle slot or strictly upper tile: nothing to write
     // tile (I, J) of the lower triangle, or its mirror (J, I) for the upper:
@@ -228,9 +234,10 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     // store writes whole 128-byte lines across 8 lanes
     const int jl = tid >> 3, r0 = tid & 7;
 
-    // threads 0..127 copy 16 bytes of each plane: half a column of P or of Q
-    const bool loader = tid < 128;
-    const int q = tid >> 6, c = (tid & 63) >> 1, h = tid & 1;
+    // each thread copies 16 bytes (half a column of P or of Q) of the chunk's
+    // planes of one parity: planes l0 + po, l0 + po + 2, ..
+    const int pc = tid & 127, po = tid >> 7;
+    const int q = pc >> 6, c = (pc & 63) >> 1, h = pc & 1;
     const int8_t *src = a.res + (q == 0 ? (size_t)(J * 32 + c) * a.ldr + I * 32 + h * 16
                                         : (size_t)(I * 32 + c) * a.ldr + J * 32 + h * 16);
     const int dst = c * 32 + h * 16;
@@ -241,27 +248,36 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
-    // the next plane's copy is in flight while this plane's limb sums run; two
-    // LDS buffers, so one barrier per plane orders both the writes before the
-    // reads and the reads of plane l - 2 before the writes of plane l
-    uint4 next = make_uint4(0, 0, 0, 0);
-    if (loader) next = *reinterpret_cast<const uint4 *>(src);
-    for (int l = 0; l < cp.n; ++l) {
-        const int buf = l & 1;
-        if (loader) {
-            *reinterpret_cast<uint4 *>(&tl[buf][q][dst]) = next;
-            if (l + 1 < cp.n) next = *reinterpret_cast<const uint4 *>(src + (size_t)(l + 1) * a.plane_bytes);
+    uint4 nx[CH / 2];
+    auto fetch = [&](int l0) {
+#pragma unroll
+        for (int x = 0; x < CH / 2; ++x) {
+            const int l = l0 + po + 2 * x;
+            nx[x] = l < cp.n ? *reinterpret_cast<const uint4 *>(src + (size_t)l * a.plane_bytes)
+                             : make_uint4(0, 0, 0, 0);
         }
+    };
+    fetch(0);
+    for (int l0 = 0; l0 < cp.n; l0 += CH) {
+        if (l0 > 0) __syncthreads();  // the previous chunk's reads are done
+#pragma unroll
+        for (int x = 0; x < CH / 2; ++x) *reinterpret_cast<uint4 *>(&tl[po + 2 * x][q][dst]) = nx[x];
         __syncthreads();
+        if (l0 + CH < cp.n) fetch(l0 + CH);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int rp = (int)tl[buf][0][jl * 32 + r0 + 8 * e];    // C+[i, j]
-            const int rm = (int)tl[buf][1][(r0 + 8 * e) * 32 + jl];  // C-[i, j] = C+[j, i]
-            const double u = (double)(rm + rp), v = (double)(rm - rp);
+        for (int t = 0; t < CH; ++t) {
+            const int l = l0 + t;
+            if (l >= cp.n) break;  // uniform
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
-                sre[e][t] = fma(u, cp.wre[l][t], sre[e][t]);
-                if (!REAL_ONLY) sim[e][t] = fma(v, cp.wim[l][t], sim[e][t]);
+            for (int e = 0; e < 4; ++e) {
+                const int rp = (int)tl[t][0][jl * 32 + r0 + 8 * e];    // C+[i, j]
+                const int rm = (int)tl[t][1][(r0 + 8 * e) * 32 + jl];  // C-[i, j] = C+[j, i]
+                const double u = (double)(rm + rp), v = (double)(rm - rp);
+#pragma unroll
+                for (int k = 0; k < T; ++k) {
+                    sre[e][k] = fma(u, cp.wre[l][k], sre[e][k]);
+                    if (!REAL_ONLY) sim[e][k] = fma(v, cp.wim[l][k], sim[e][k]);
+                }
             }
         }
     }
