@@ -57,9 +57,13 @@ __device__ inline typename OutT<OT>::type finish(const double (&sre)[T], const d
 
 // MODE 0: ZGEMM / CGEMM output.  MODE 3: exact Gaussian integers (int64).
 // MODE 4: residue hook (per-modulus 2M post output).  Each thread owns R = 4
-// consecutive rows of one column: one dword per plane.
+// consecutive rows of one column: one dword per plane.  Up to three limbs
+// the row exponents are fetched before the limb sums and the kernel is held
+// to 80 registers (six waves per SIMD; it needs 81 otherwise); with more
+// limbs both would cost occupancy or spills, and the exponents are read when
+// the rows are finished.
 template <int T, int MODE, ElemType OT>
-__global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
+__global__ __launch_bounds__(256, T <= 3 ? 6 : 1) void crt_kernel(CrtArgs a, CrtParams cp) {
     constexpr int R = 4;
     const int rows_per_block = 256 * R;
     const int mblocks = (a.m + rows_per_block - 1) / rows_per_block;
@@ -103,6 +107,17 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
             }
         }
         return;
+    }
+
+    // the exponents of the thread's rows and column, fetched before the limb
+    // sums so that their latency is hidden behind them (E holds every padded
+    // row, and i0, a multiple of 4, is below m or replaced by row 0)
+    constexpr bool EARLY = MODE == 0 && T <= 3;
+    int ev[R] = {}, fj = 0;
+    if constexpr (EARLY) {
+        const int4 e4 = *reinterpret_cast<const int4 *>(a.E + (i0 < a.m ? i0 : 0));
+        ev[0] = e4.x; ev[1] = e4.y; ev[2] = e4.z; ev[3] = e4.w;
+        fj = a.F[j];
     }
 
     double sre[R][T], sim[R][T];
@@ -190,7 +205,8 @@ __global__ __launch_bounds__(256) void crt_kernel(CrtArgs a, CrtParams cp) {
                                            (unsigned __int128)((uint64_t)ma * (uint64_t)mb);
             if (need > (unsigned __int128)(uint64_t)h) atomicOr(a.status, kStatusOverflow);
         } else {
-            const int ei = a.E[i], fj = a.F[j];
+            const int ei = EARLY ? ev[e] : a.E[i];
+            if constexpr (!EARLY) fj = a.F[j];
             const SV v = finish<T, OT>(sre[e], sim[e], cp, ei == INT32_MIN || fj == INT32_MIN, ei + fj + a.scale_bias);
             if constexpr (STAGE) stage[threadIdx.x * R + e] = v;
             else reinterpret_cast<SV *>(a.c)[(size_t)i + (size_t)j * a.ldc] = v;
