@@ -233,9 +233,11 @@ __global__ __launch_bounds__(256, T <= 3 ? 6 : 1) void crt_kernel(CrtArgs a, Crt
 // run.  The real-only form, light on arithmetic, waits on memory and takes 8
 // planes per chunk; the complex form issues twice the limb sums and takes 4,
 // whose staging registers cost less occupancy (measured: 8 planes or copies
-// straight into LDS were slower for it).
+// straight into LDS were slower for it).  The rows' exponents are fetched
+// before the limb sums; the complex form is held to 80 registers up to three
+// limbs (six waves per SIMD) and 96 with four (five).
 template <int T, bool REAL_ONLY>
-__global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
+__global__ __launch_bounds__(256, REAL_ONLY ? 1 : (T <= 3 ? 6 : 5)) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     constexpr int CH = REAL_ONLY ? 8 : 4;  // planes per chunk
     // [plane of the chunk][P = C+ tile (I, J), Q = C+ tile (J, I)], column-major 32 x 32
     __shared__ __attribute__((aligned(16))) int8_t tl[CH][2][32 * 32];
@@ -257,6 +259,13 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     const int8_t *src = a.res + (q == 0 ? (size_t)(J * 32 + c) * a.ldr + I * 32 + h * 16
                                         : (size_t)(I * 32 + c) * a.ldr + J * 32 + h * 16);
     const int dst = c * 32 + h * 16;
+
+    // the exponents of the thread's rows and column, fetched before the limb
+    // sums (E holds every padded row, and the tiles cover no more)
+    int ev[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ev[e] = a.E[I * 32 + r0 + 8 * e];
+    const int ej = a.E[J * 32 + jl];
 
     double sre[4][T], sim[4][T];
 #pragma unroll
@@ -303,7 +312,7 @@ __global__ __launch_bounds__(256) void crt_sym_kernel(CrtArgs a, CrtParams cp) {
     for (int e = 0; e < 4; ++e) {
         const int i = I * 32 + r0 + 8 * e;
         if (i >= a.n || j >= a.n || (a.upper ? i > j : i < j)) continue;
-        const int ei = a.E[i], ej = a.E[j];
+        const int ei = ev[e];
         const bool bad = ei == INT32_MIN || ej == INT32_MIN;
         const int sc = ei + ej + a.scale_bias;
         if (REAL_ONLY) {
