@@ -20,6 +20,17 @@ constexpr double kTwo40 = 1099511627776.0;
 constexpr double kTwo80 = 1208925819614629174706176.0;
 constexpr double kTwo120 = 1329227995784915872903807060280344576.0;
 
+// A constant held in scalar registers on the device: a literal operand only
+// fits the two-operand fma, which costs a register copy whenever its addend
+// is still needed, while a scalar-register operand fits the three-operand
+// form.  The empty asm only pins the value there; it emits no instruction.
+O2M_HD inline double in_sreg(double x) {
+#ifdef __HIP_DEVICE_COMPILE__
+    asm("" : "+s"(x));
+#endif
+    return x;
+}
+
 O2M_HD inline int64_t bits_of_f64(double x) { return __builtin_bit_cast(int64_t, x); }
 O2M_HD inline double f64_of_bits(int64_t b) { return __builtin_bit_cast(double, b); }
 
@@ -88,15 +99,16 @@ O2M_HD inline double round_top3(double a, double b, double y) {
 // (at |d0| = 2^39 below a power of two, a tie that goes to s, whose
 // significand is even).
 O2M_HD inline double round3_rn(double c0, double c1, double c2) {
+    const double two40 = in_sreg(kTwo40);
     const double h0 = rint(c0 * 0x1p-40);
-    const double d0 = fma(-h0, kTwo40, c0);
+    const double d0 = fma(-h0, two40, c0);
     c1 += h0;
     const double h1 = rint(c1 * 0x1p-40);
-    const double d1 = fma(-h1, kTwo40, c1);
+    const double d1 = fma(-h1, two40, c1);
     c2 += h1;
-    const double a = c2 * kTwo80;
-    const double s = fma(d1, kTwo40, a);
-    const double e = fma(d1, kTwo40, -(s - a));
+    const double a = c2 * in_sreg(kTwo80);
+    const double s = fma(d1, two40, a);
+    const double e = fma(d1, two40, -(s - a));
     const double n = fma(2.0, e, s);
     return n - s == 2.0 * e && e * d0 > 0.0 ? n : s + d0;
 }
@@ -223,8 +235,9 @@ struct LimbWords {
 // the lifted limbs c_t = S_t - q M_t (exact).
 template <int T>
 O2M_HD inline void lift_limbs(const double (&S)[T], const double *mlimb, double inv_m, double (&c)[T]) {
+    const double two40 = in_sreg(kTwo40);
     double X = S[T - 1];
-    for (int t = T - 2; t >= 0; --t) X = fma(X, kTwo40, S[t]);
+    for (int t = T - 2; t >= 0; --t) X = fma(X, two40, S[t]);
     const double q = rint(X * inv_m);
     for (int t = 0; t < T; ++t) c[t] = fma(-q, mlimb[t], S[t]);
 }
@@ -266,10 +279,11 @@ O2M_HD inline double ro_digits4(double d0, double d1, double d2, double d3) {
 template <int T>
 O2M_HD inline void top3_of(double (&c)[T], double &a, double &b, double &low) {
     static_assert(T >= 4 && T <= 6, "three-term reduction for four to six limbs");
+    const double two40 = in_sreg(kTwo40);
 #pragma unroll
     for (int t = 0; t + 1 < T; ++t) {
         const double h = rint(c[t] * (1.0 / kTwo40));
-        c[t] = fma(-h, kTwo40, c[t]);
+        c[t] = fma(-h, two40, c[t]);
         c[t + 1] += h;
     }
     if constexpr (T == 6) {
@@ -312,7 +326,7 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
     lift_limbs<T>(S, mlimb, inv_m, c);
     double x;
     if constexpr (T == 2) {
-        x = fma(c[1], kTwo40, c[0]);     // one rounding of an exact sum
+        x = fma(c[1], in_sreg(kTwo40), c[0]);     // one rounding of an exact sum
     } else if constexpr (T == 3) {
         x = round3_rn(c[0], c[1], c[2]);
     } else {

@@ -329,12 +329,17 @@ __global__ __launch_bounds__(256, REAL_ONLY ? 1 : (T <= 3 ? 6 : 5)) void crt_sym
 template <int T>
 hipError_t launch_t(int mode, ElemType ot, const CrtArgs &ca, const CrtParams &cp, hipStream_t st) {
     if (mode == 1 || mode == 2) {
-        if (T > 4 || cp.n2 != cp.n) return hipErrorInvalidValue;  // symmetric ops: 2M moduli only
-        const long blocks = sym_grid((ca.n + 31) / 32);
-        if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-        if (mode == 1) crt_sym_kernel<T, false><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-        else crt_sym_kernel<T, true><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
-        return hipGetLastError();
+        // symmetric ops: 2M moduli only, so at most 22 moduli and four limbs
+        if constexpr (T > 4) {
+            return hipErrorInvalidValue;
+        } else {
+            if (cp.n2 != cp.n) return hipErrorInvalidValue;
+            const long blocks = sym_grid((ca.n + 31) / 32);
+            if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+            if (mode == 1) crt_sym_kernel<T, false><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+            else crt_sym_kernel<T, true><<<(unsigned)blocks, 256, 0, st>>>(ca, cp);
+            return hipGetLastError();
+        }
     }
     // 4 rows of one column per thread, 1024 rows per workgroup
     const long blocks = (long)((ca.m + 1023) / 1024) * ca.n;
