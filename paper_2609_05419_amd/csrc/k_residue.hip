@@ -28,6 +28,8 @@
 // 16 read + 2N written (8 + 2N for fp32 input).
 #include "o2m_internal.h"
 
+#include <type_traits>
+
 namespace o2m {
 namespace {
 
@@ -126,7 +128,7 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
     constexpr int PT = per_thread<D>();
     constexpr int kHalves = 16 / PT;                          // waves per fragment
     const int lane = threadIdx.x & 63;
-    const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));  // wave-uniform
     const int frag = wave / kHalves, half = wave % kHalves;   // one fragment per kHalves waves
     const int frows = rows_pad / kFragRows;                   // fragments along rows
     const int fks = kblocks;                                  // fragments along k
@@ -143,15 +145,28 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
     const int kk0 = fk * kStageK + (chunk >> 4) * 16 + part * PT;
 
     // ---- load and quantize (step 3) -------------------------------------
+    // A wave whose fragment (16 rows x 64 k) lies inside the operand takes
+    // every load unguarded, so all of them are in flight before the first is
+    // used; the guarded form is taken at the edges only.  (With a per-lane
+    // guard around each load the compiler moves the quantization of the value
+    // into the guarded branch, where it must wait for that load: the loads
+    // then went out one at a time.)
     typedef typename Digit<D>::type DT;
     DT xr[D][PT], xi[D][PT];
+    const bool inner = fr * kFragRows + kFragRows <= rows && fk * kStageK + kStageK <= k &&
+                       (MODE != 2 || fk * kStageK + kStageK + khalf <= kreal);
+    // the row's exponent is fetched first and used once the entries' loads
+    // are issued (every padded row has an entry)
+    int erow = 0;
+    if constexpr (SCALED) erow = E[r];
     int sh = 0;
-    bool live = r < rows;
-    if (SCALED && live) {
-        const int e = E[r];
-        if (e == INT32_MIN) live = false;    // non-finite row: output masked later
-        else sh = shift - e;
-    }
+    bool live = r < rows;                    // bounds only until settle()
+    auto settle = [&]() {
+        if constexpr (SCALED) {
+            live = live && erow != INT32_MIN;  // non-finite row: output masked later
+            sh = shift - erow;
+        }
+    };
     auto put = [&](int e, double vr, double vi) {
         if (!live) vr = vi = 0.0;
         if (conj) vi = -vi;                  // conjugated operand: exact
@@ -162,72 +177,91 @@ __global__ __launch_bounds__(256, D == 1 ? 3 : 1) void residue_kernel(const void
         split_digits<D, PT>(vr, xr, e);
         split_digits<D, PT>(vi, xi, e);
     };
-    if constexpr (PAIRS && MODE == 0) {
-        static_assert(ET == kF32 && PT == 16, "pairs of complex fp32 rows, one lane chunk per lane");
-        const bool odd = lane & 1;
-        const int re = r - (int)odd;                 // the pair's even row
-        const float2 *Xa = reinterpret_cast<const float2 *>(X);
-        float4 v[8];
+    auto load_all = [&](auto edge) {
+        constexpr bool EDGE = decltype(edge)::value;
+        if constexpr (PAIRS && MODE == 0) {
+            static_assert(ET == kF32 && PT == 16, "pairs of complex fp32 rows, one lane chunk per lane");
+            const bool odd = lane & 1;
+            const int re = r - (int)odd;                 // the pair's even row
+            const float2 *Xa = reinterpret_cast<const float2 *>(X);
+            float4 v[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int kk = kk0 + (odd ? 8 : 0) + j;
-            v[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if (kk < k) {
-                if (re + 1 < rows) {
+            for (int j = 0; j < 8; ++j) {
+                const int kk = kk0 + (odd ? 8 : 0) + j;
+                v[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                if (!EDGE) {
                     v[j] = *reinterpret_cast<const float4 *>(Xa + (size_t)re + (size_t)kk * ld);
-                } else if (re < rows) {
-                    const float2 t = Xa[(size_t)re + (size_t)kk * ld];
-                    v[j].x = t.x;
-                    v[j].y = t.y;
+                } else if (kk < k) {
+                    if (re + 1 < rows) {
+                        v[j] = *reinterpret_cast<const float4 *>(Xa + (size_t)re + (size_t)kk * ld);
+                    } else if (re < rows) {
+                        const float2 t = Xa[(size_t)re + (size_t)kk * ld];
+                        v[j].x = t.x;
+                        v[j].y = t.y;
+                    }
                 }
             }
-        }
+            settle();
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            // the even lane passes on its odd row's half, the odd lane its even row's
-            const float rx = __shfl_xor(odd ? v[j].x : v[j].z, 1, 64);
-            const float ry = __shfl_xor(odd ? v[j].y : v[j].w, 1, 64);
-            put(j, odd ? rx : v[j].x, odd ? ry : v[j].y);
-            put(8 + j, odd ? v[j].z : rx, odd ? v[j].w : ry);
-        }
-    } else if constexpr (PAIRS) {
-        static_assert(MODE == 1 && ET == kF32, "pairs of complex fp32 entries along a column");
-        const float2 *Xc = reinterpret_cast<const float2 *>(X) + (size_t)r * ld;
-#pragma unroll
-        for (int e = 0; e < PT; e += 2) {
-            const int kk = kk0 + e;
-            float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if (live && kk + 1 < k) {
-                v = *reinterpret_cast<const float4 *>(Xc + kk);
-            } else if (live && kk < k) {
-                const float2 t = Xc[kk];
-                v.x = t.x;
-                v.y = t.y;
+            for (int j = 0; j < 8; ++j) {
+                // the even lane passes on its odd row's half, the odd lane its even row's
+                const float rx = __shfl_xor(odd ? v[j].x : v[j].z, 1, 64);
+                const float ry = __shfl_xor(odd ? v[j].y : v[j].w, 1, 64);
+                put(j, odd ? rx : v[j].x, odd ? ry : v[j].y);
+                put(8 + j, odd ? v[j].z : rx, odd ? v[j].w : ry);
             }
-            put(e, (double)v.x, (double)v.y);
-            put(e + 1, (double)v.z, (double)v.w);
-        }
-    } else {
+        } else if constexpr (PAIRS) {
+            static_assert(MODE == 1 && ET == kF32, "pairs of complex fp32 entries along a column");
+            const float2 *Xc = reinterpret_cast<const float2 *>(X) + (size_t)r * ld;
+            float4 v[PT / 2];
 #pragma unroll
-        for (int e = 0; e < PT; ++e) {
-            const int kk = kk0 + e;
-            double vr = 0.0, vi = 0.0;
-            if (live && kk < k) {
-                if (MODE == 0) {
-                    const double2 v = Load<ET>::get(X, (size_t)r + (size_t)kk * ld);
-                    vr = v.x; vi = v.y;
-                } else if (MODE == 1) {
-                    const double2 v = Load<ET>::get(X, (size_t)kk + (size_t)r * ld);
-                    vr = v.x; vi = v.y;
-                } else {
-                    const double *Xr = reinterpret_cast<const double *>(X);
-                    vr = Xr[(size_t)r + (size_t)kk * ld];
-                    if (kk + khalf < kreal) vi = Xr[(size_t)r + (size_t)(kk + khalf) * ld];
+            for (int e = 0; e < PT; e += 2) {
+                const int kk = kk0 + e;
+                v[e / 2] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                if (!EDGE) {
+                    v[e / 2] = *reinterpret_cast<const float4 *>(Xc + kk);
+                } else if (live && kk + 1 < k) {
+                    v[e / 2] = *reinterpret_cast<const float4 *>(Xc + kk);
+                } else if (live && kk < k) {
+                    const float2 t = Xc[kk];
+                    v[e / 2].x = t.x;
+                    v[e / 2].y = t.y;
                 }
             }
-            put(e, vr, vi);
+            settle();
+#pragma unroll
+            for (int e = 0; e < PT; e += 2) {
+                put(e, (double)v[e / 2].x, (double)v[e / 2].y);
+                put(e + 1, (double)v[e / 2].z, (double)v[e / 2].w);
+            }
+        } else {
+            double vr[PT], vi[PT];
+#pragma unroll
+            for (int e = 0; e < PT; ++e) {
+                const int kk = kk0 + e;
+                vr[e] = 0.0;
+                vi[e] = 0.0;
+                if (!EDGE || (live && kk < k)) {
+                    if (MODE == 0) {
+                        const double2 v = Load<ET>::get(X, (size_t)r + (size_t)kk * ld);
+                        vr[e] = v.x; vi[e] = v.y;
+                    } else if (MODE == 1) {
+                        const double2 v = Load<ET>::get(X, (size_t)kk + (size_t)r * ld);
+                        vr[e] = v.x; vi[e] = v.y;
+                    } else {
+                        const double *Xr = reinterpret_cast<const double *>(X);
+                        vr[e] = Xr[(size_t)r + (size_t)kk * ld];
+                        if (!EDGE || kk + khalf < kreal) vi[e] = Xr[(size_t)r + (size_t)(kk + khalf) * ld];
+                    }
+                }
+            }
+            settle();
+#pragma unroll
+            for (int e = 0; e < PT; ++e) put(e, vr[e], vi[e]);
         }
-    }
+    };
+    if (__builtin_expect(inner, 1)) load_all(std::false_type());
+    else load_all(std::true_type());
 
     // ---- residues and 2M pre per modulus (step 4, eq. 2m-pre) -------------
     int8_t *dst_p = planes + plane_offset(r, kk0 + kofs_p * kStageK, plane_kblocks);
