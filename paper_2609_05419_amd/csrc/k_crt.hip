@@ -273,22 +273,32 @@ __global__ __launch_bounds__(256, REAL_ONLY ? 1 : (T <= 3 ? 6 : 5)) void crt_sym
 #pragma unroll
         for (int t = 0; t < T; ++t) { sre[e][t] = 0.0; sim[e][t] = 0.0; }
 
-    uint4 nx[CH / 2];
+    // every copy is taken, from plane n - 1 past the last one (never summed),
+    // so that none waits inside a branch; the chunk is held in one vector
+    // value, which stays in registers
+    typedef unsigned int Stage __attribute__((ext_vector_type(2 * CH)));
+    Stage nx;
     auto fetch = [&](int l0) {
 #pragma unroll
         for (int x = 0; x < CH / 2; ++x) {
-            const int l = l0 + po + 2 * x;
-            nx[x] = l < cp.n ? *reinterpret_cast<const uint4 *>(src + (size_t)l * a.plane_bytes)
-                             : make_uint4(0, 0, 0, 0);
+            const int l = min(l0 + po + 2 * x, cp.n - 1);
+            const uint4 w = *reinterpret_cast<const uint4 *>(src + (size_t)l * a.plane_bytes);
+            nx[4 * x] = w.x;
+            nx[4 * x + 1] = w.y;
+            nx[4 * x + 2] = w.z;
+            nx[4 * x + 3] = w.w;
         }
     };
     fetch(0);
     for (int l0 = 0; l0 < cp.n; l0 += CH) {
         if (l0 > 0) __syncthreads();  // the previous chunk's reads are done
 #pragma unroll
-        for (int x = 0; x < CH / 2; ++x) *reinterpret_cast<uint4 *>(&tl[po + 2 * x][q][dst]) = nx[x];
+        for (int x = 0; x < CH / 2; ++x)
+            *reinterpret_cast<uint4 *>(&tl[po + 2 * x][q][dst]) =
+                make_uint4(nx[4 * x], nx[4 * x + 1], nx[4 * x + 2], nx[4 * x + 3]);
         __syncthreads();
         if (l0 + CH < cp.n) fetch(l0 + CH);
+        asm volatile("" ::: "memory");  // the next chunk's loads stay ahead of the sums
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
             const int l = l0 + t;
