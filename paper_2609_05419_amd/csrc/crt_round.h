@@ -319,7 +319,10 @@ O2M_HD inline void top3_of(double (&c)[T], double &a, double &b, double &low) {
 // 2^sc,
 // which is exact unless the result is subnormal; such results (and those that
 // underflow to zero) are rounded again from the exact integer, held as 192 or
-// 256 bits, at the subnormal quantum.
+// 256 bits, at the subnormal quantum.  A value just below 2^-1022 can round
+// to 2^-1022 itself in the scaling (the 53-bit value ties on the subnormal
+// grid), so |r| = 2^-1022 takes the exact path too; rounding is monotone, so
+// every exact value below 2^-1022 gives |r| <= 2^-1022.
 template <int T>
 O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, double inv_m, int sc) {
     double c[T];
@@ -335,7 +338,7 @@ O2M_HD inline double lift_round(const double (&S)[T], const double *mlimb, doubl
         x = round_top3(a, b, low);
     }
     const double r = ldexp(x, sc);
-    if (x == 0.0 || !(fabs(r) < 0x1p-1022)) return r;
+    if (x == 0.0 || !(fabs(r) <= 0x1p-1022)) return r;
     return round_words<LimbWords<T>::value>(words_of<T>(c), sc);
 }
 

@@ -265,6 +265,25 @@ def test_many_limb_rounding_via_three_terms(lib, T, fmt):
             assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, limbs, sc)
 
 
+@pytest.mark.parametrize("T", [2, 3, 4, 5, 6])
+def test_normal_boundary_ties_round_once(lib, T):
+    """c = 2^t - 2^(t-53) - 1 at 2^(-1022-t): c 2^sc lies just below 2^-1022
+    and RN53(c) 2^sc = 2^-1022 - 2^-1075 ties on the subnormal grid, so the
+    scaled 53-bit value rounds to 2^-1022; the one rounding of c 2^sc is the
+    largest subnormal.  (Returning the scaled value whenever it is not below
+    2^-1022 failed every case here.)"""
+    top = 40 * T - 10
+    for s in (1, -1):
+        c = s * ((1 << top) - (1 << (top - 53)) - 1)
+        sc = -1022 - top
+        assert O.round_scaled(c, sc, "f64") == s * (2.0 ** -1022 - 2.0 ** -1074)
+        rng = random.Random(T)
+        limbs = split_limbs(c, T, rng)
+        arr = np.array(limbs, dtype=np.float64)
+        got = lib.t_round_lifted(arr.ctypes.data, T, sc, 0)
+        assert np.float64(got).view(np.uint64) == np.float64(s * (2.0 ** -1022 - 2.0 ** -1074)).view(np.uint64)
+
+
 @pytest.mark.parametrize("T,bits", [(4, 150), (5, 190), (6, 245)])
 def test_multiword_rounding(lib, T, bits):
     rng = random.Random(T)

@@ -85,6 +85,24 @@ def test_zgemm_subnormal_ties_once(o2m, N, k):
     assert (np.abs(got[7, :].real) < 2.0 ** -1022).any()
 
 
+@pytest.mark.parametrize("N", [16, 22])
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_zgemm_normal_boundary_rounds_once(o2m, N, sign):
+    """An exact product just below 2^-1022, (2^57 - 17) 2^-1079, whose 53-bit
+    rounding (2^53 - 1) 2^-1075 ties on the subnormal grid: scaling that value
+    would give 2^-1022, the one rounding gives the largest subnormal."""
+    k = 2
+    pA, _ = O.shifts("max", O.moduli_set(N), k)
+    assert pA >= 57                         # every entry below quantizes exactly
+    ar = np.array([[sign * (2 ** 53 - 1) * 2.0 ** -540, -sign * 2.0 ** -544]], dtype=np.complex128)
+    bc = np.array([[2.0 ** -535], [2.0 ** -535]], dtype=np.complex128)
+    a, b = embed(40, 30, k, 900 + N, np.complex128, [(5, 7, ar, bc)])
+    print(f"[rounding] zgemm normal boundary N={N} sign={sign}", flush=True)
+    got = host(o2m.zgemm_2m(to_dev(a), to_dev(b), n_moduli=N))
+    assert same_bits(got, O.oq_zgemm(a, b, N))
+    assert got[5, 7].real == sign * (2.0 ** -1022 - 2.0 ** -1074)
+
+
 @pytest.mark.parametrize("N", [8, 16, 20])
 def test_zherk_subnormal_outputs(o2m, N):
     n, k = 60, 40

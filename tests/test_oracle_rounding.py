@@ -239,6 +239,25 @@ def test_zgemm_oracle_fp64_subnormal_tie(N, k):
     assert math.ldexp(-float((1 << L) + (1 << (L - j)) + 1), E + F - pA - pB) == -(2.0 ** (j - 1075))
 
 
+@pytest.mark.parametrize("N", [16, 22])
+@pytest.mark.parametrize("sign", [1, -1])
+def test_zgemm_oracle_normal_boundary_tie(N, sign):
+    """Exact product (2^57 - 17) 2^-1079 = 2^-1022 - 2^-1075 - 2^-1079: the
+    nearest values are 2^-1022 - 2^-1074 (2^-1075 - 2^-1079 away) and 2^-1022
+    (2^-1075 + 2^-1079 away), so the one rounding gives the largest subnormal,
+    while rounding to 53 bits first ((2^53 - 1) 2^-1075, a tie on the
+    subnormal grid) and then scaling would give 2^-1022."""
+    a = np.array([[sign * (2 ** 53 - 1) * 2.0 ** -540, -sign * 2.0 ** -544]], dtype=np.complex128)
+    b = np.array([[2.0 ** -535], [2.0 ** -535]], dtype=np.complex128)
+    exact = (Fraction(a[0, 0].real) + Fraction(a[0, 1].real)) * Fraction(b[0, 0].real)
+    assert exact == sign * Fraction(2 ** 57 - 17, 2 ** 1079)
+    want = sign * (2.0 ** -1022 - 2.0 ** -1074)
+    assert abs(exact - Fraction(want)) < abs(exact - Fraction(sign * 2.0 ** -1022))
+    assert math.ldexp(sign * float(2 ** 57 - 17), -1079) == sign * 2.0 ** -1022   # the double rounding
+    got = O.oq_zgemm(a, b, N)[0, 0]
+    assert got.real == want and got.imag == 0
+
+
 def test_cgemm_oracle_matches_enumerated_rounding_of_exact_integers():
     """Random CGEMM entries: the oracle's fp32 output is the enumerated
     nearest fp32 of the exact scaled integer product."""
