@@ -284,6 +284,26 @@ def test_normal_boundary_ties_round_once(lib, T):
         assert np.float64(got).view(np.uint64) == np.float64(s * (2.0 ** -1022 - 2.0 ** -1074)).view(np.uint64)
 
 
+@pytest.mark.parametrize("T", [2, 3, 4, 5, 6])
+def test_rounding_near_format_boundaries(lib, T):
+    """Values c 2^sc whose 24- or 53-bit patterns sit at or next to a tie,
+    scaled to just below 2^-126, 2^-127, 2^-140, 2^-149, 2^-150 and 2^-1022
+    (fp32's normal, subnormal and underflow boundaries, fp64's normal one),
+    into fp32 and fp64: one rounding each, as the oracle rounds."""
+    top = 40 * T - 10
+    for s in (1, -1):
+        for p in (24, 53):
+            for d in (-1, 0, 1, 2):
+                c = s * ((1 << top) - (1 << (top - p)) + d)
+                limbs = split_limbs(c, T, random.Random(top + p + d))
+                arr = np.array(limbs, dtype=np.float64)
+                for tgt in (-126, -127, -140, -149, -150, -1022):
+                    for fmt in ("f32", "f64"):
+                        got = lib.t_round_lifted(arr.ctypes.data, T, tgt - top, int(fmt == "f32"))
+                        want = narrow(O.round_scaled(c, tgt - top, fmt), fmt)
+                        assert np.float64(got).view(np.uint64) == np.float64(want).view(np.uint64), (c, tgt, fmt)
+
+
 @pytest.mark.parametrize("T,bits", [(4, 150), (5, 190), (6, 245)])
 def test_multiword_rounding(lib, T, bits):
     rng = random.Random(T)
