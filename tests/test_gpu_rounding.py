@@ -103,6 +103,28 @@ def test_zgemm_normal_boundary_rounds_once(o2m, N, sign):
     assert got[5, 7].real == sign * (2.0 ** -1022 - 2.0 ** -1074)
 
 
+@pytest.mark.parametrize("N", [16, 22])
+def test_symmetric_normal_boundary_rounds_once(o2m, N):
+    """The same tie through the symmetric CRT: with row 0 = [b, b] and row 1 =
+    [a1, a2], entry (1, 0) of A A^H (and of the real A A^T, whose half-k
+    complex form has z_i = a_i0 + i a_i1) is (a1 + a2) b."""
+    rng = np.random.default_rng(950 + N)
+    a = rng.standard_normal((6, 2))
+    a[0, :] = 2.0 ** -535
+    a[1, 0], a[1, 1] = (2 ** 53 - 1) * 2.0 ** -540, -(2.0 ** -544)
+    a = np.asfortranarray(a)
+    low = np.tril(np.ones((6, 6), dtype=bool))
+    want = 2.0 ** -1022 - 2.0 ** -1074
+    print(f"[rounding] zherk / dsyrk normal boundary N={N}", flush=True)
+    ac = np.asfortranarray(a.astype(np.complex128))
+    got = host(o2m.zherk_2m(to_dev(ac), n_moduli=N))
+    assert same_bits(got[low], O.oq_zherk(ac, N)[low])
+    assert got[1, 0].real == want
+    got = host(o2m.dsyrk_2m(to_dev(a), n_moduli=N))
+    assert same_bits(got[low], O.oq_dsyrk(a, N)[low])
+    assert got[1, 0] == want
+
+
 @pytest.mark.parametrize("N", [8, 16, 20])
 def test_zherk_subnormal_outputs(o2m, N):
     n, k = 60, 40
