@@ -288,8 +288,9 @@ def test_normal_boundary_ties_round_once(lib, T):
 def test_rounding_near_format_boundaries(lib, T):
     """Values c 2^sc whose 24- or 53-bit patterns sit at or next to a tie,
     scaled to just below 2^-126, 2^-127, 2^-140, 2^-149, 2^-150 and 2^-1022
-    (fp32's normal, subnormal and underflow boundaries, fp64's normal one),
-    into fp32 and fp64: one rounding each, as the oracle rounds."""
+    (fp32's normal, subnormal and underflow boundaries, fp64's normal one)
+    and 2^127, 2^128, 2^1023, 2^1024 (the largest binades and the overflow
+    thresholds), into fp32 and fp64: one rounding each, as the oracle rounds."""
     top = 40 * T - 10
     for s in (1, -1):
         for p in (24, 53):
@@ -297,7 +298,7 @@ def test_rounding_near_format_boundaries(lib, T):
                 c = s * ((1 << top) - (1 << (top - p)) + d)
                 limbs = split_limbs(c, T, random.Random(top + p + d))
                 arr = np.array(limbs, dtype=np.float64)
-                for tgt in (-126, -127, -140, -149, -150, -1022):
+                for tgt in (-126, -127, -140, -149, -150, -1022, 127, 128, 1023, 1024):
                     for fmt in ("f32", "f64"):
                         got = lib.t_round_lifted(arr.ctypes.data, T, tgt - top, int(fmt == "f32"))
                         want = narrow(O.round_scaled(c, tgt - top, fmt), fmt)
